@@ -1,0 +1,244 @@
+"""fp64 CPU oracle for one EigenPro 2.0 iteration — TEST INFRASTRUCTURE.
+
+Used only by ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
+``cpu_baseline`` leg; never by the product path. It shares no code with the
+HIP library. Inputs may be float32 arrays (the synthetic data); every
+computation converts them to float64 first.
+
+Paper: Ma & Belkin, "Kernel machines that adapt to GPUs for effective large
+batch training" (SysML 2019, arXiv 1806.06144).
+
+What each function follows
+--------------------------
+kernel_matrix      Appendix B: Gaussian exp(-|x-z|^2 / (2 sigma^2)) and
+                   Laplacian exp(-|x-z| / sigma).
+setup              Algorithm 1 (initialisation: subsample r, top eigensystem
+                   of K_s); Section 4 (Nystrom extension: lambda_i ~ sigma_i/s,
+                   D = Sigma^-1 (1 - sigma_q Sigma^-1)); Section 3, Step 2
+                   (beta(K_P) as the largest k_P(x, x) over subsample points,
+                   lambda_1(K_P) = lambda_q); Section 2 (critical batch
+                   m* = beta / lambda_1).
+step_coefficient   Section 3, Step 3 and Appendix C, read as the optimal
+                   per-coordinate step c(m) = 1 / (beta + (m - 1) lambda_q)
+                   (see "Readings" below).
+step               Algorithm 1, steps 1-5, in matrix form.
+step_pointwise     Algorithm 1, steps 2-5, one point and one coordinate at a
+                   time (pure Python loops; tiny cases only).
+predict            Section 2: f(z) = sum_i alpha_i k(x_i, z).
+interpolant        Section 2: alpha* = K^{-1} y, the unique interpolating
+                   solution every iteration converges to.
+
+Readings of the paper (shared with the HIP path by construction)
+----------------------------------------------------------------
+* q = k + 1: the top k + 1 eigenpairs of K_s are computed; V holds the top k
+  eigenvectors and sigma_{k+1} is the flattening level. The paper's D has
+  D_qq = 0, so this is the paper's update with q = k + 1.
+* Step size: Algorithm 1 writes eta * 2/m and Section 3 Step 3 sets
+  eta = m / beta, which puts the per-coordinate step at 2/beta, the edge of
+  stability. Table 5's (m, eta) pairs satisfy m / eta ~ 2, i.e. a
+  per-coordinate step of about 1/(2 beta) at m = m*, which is the optimal
+  step 1 / (beta + (m - 1) lambda) of the interpolation analysis the paper
+  relies on (Appendix C's denominator). The oracle uses
+  c(m) = 1 / (beta_G + (m - 1) lambda_{k+1}) for both coordinate blocks, with
+  the m of the batch at hand (a short last batch uses its own size).
+* beta(K_G) is taken over the s subsample points, where k_P(x, x) has the
+  closed form 1 - sum_j (sigma_j - sigma_{k+1}) V_ij^2.
+* Both coordinate-block updates use the residual of the pre-step model and
+  add; rows in both the batch and the subsample receive both.
+* Squared distances use |a|^2 + |b|^2 - 2 a.b in float64 (a matrix product
+  as a library step), clamped at zero so that the square root of the
+  Laplacian kernel is defined when rounding makes the expansion negative.
+* Sums over the n centres are accumulated block by block over rows of X.
+
+Parity pins live in tests/test_oracle_*.py.
+"""
+
+from dataclasses import dataclass
+
+import numpy as np
+import scipy.linalg
+
+GAUSSIAN = 0
+LAPLACIAN = 1
+
+_BLOCK = 16384
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+def sq_dist(A, B):
+    """All pairwise |a - b|^2 (float64), rows of A against rows of B."""
+    A = _f64(A)
+    B = _f64(B)
+    an = np.einsum("ij,ij->i", A, A)
+    bn = np.einsum("ij,ij->i", B, B)
+    d2 = an[:, None] + bn[None, :] - 2.0 * (A @ B.T)
+    np.maximum(d2, 0.0, out=d2)
+    return d2
+
+
+def kernel_matrix(A, B, kernel, bandwidth):
+    """[k(a_i, b_j)] in float64 (Appendix B kernels)."""
+    d2 = sq_dist(A, B)
+    if kernel == GAUSSIAN:
+        return np.exp(-d2 / (2.0 * float(bandwidth) ** 2))
+    if kernel == LAPLACIAN:
+        return np.exp(-np.sqrt(d2) / float(bandwidth))
+    raise ValueError(f"unknown kernel {kernel!r}")
+
+
+def _kernel_times(Q, X, W, kernel, bandwidth, block=_BLOCK):
+    """sum_i k(q, x_i) W_i for every row q of Q, over all rows x_i of X,
+    accumulated block by block over the rows of X."""
+    Q = _f64(Q)
+    out = np.zeros((Q.shape[0], W.shape[1]), dtype=np.float64)
+    for a in range(0, X.shape[0], block):
+        b = min(X.shape[0], a + block)
+        out += kernel_matrix(Q, X[a:b], kernel, bandwidth) @ _f64(W[a:b])
+    return out
+
+
+@dataclass
+class OracleState:
+    """Setup products of Algorithm 1's initialisation and Section 3."""
+    X: np.ndarray            # n x d training features (any float dtype)
+    kernel: int
+    bandwidth: float
+    r: np.ndarray            # s subsample indices
+    Xs: np.ndarray           # s x d, float64
+    sigma: np.ndarray        # top k+1 eigenvalues of K_s, descending
+    V: np.ndarray            # s x k top eigenvectors
+    D: np.ndarray            # k: (1 - sigma_{k+1}/sigma_i) / sigma_i
+    beta: float              # beta(K_G)
+    lam: float               # lambda_{k+1} = sigma_{k+1} / s
+    m_star: float            # beta / lambda
+    m: int                   # min(n, max(1, floor(m*)))
+
+    @property
+    def s(self):
+        return self.r.shape[0]
+
+    @property
+    def k(self):
+        return self.V.shape[1]
+
+    @property
+    def n(self):
+        return self.X.shape[0]
+
+
+def beta_closed_form(sigma, V):
+    """max over subsample points of k_P(x_ri, x_ri) = 1 - sum_j (sigma_j -
+    sigma_{k+1}) V_ij^2 (Section 3 Step 2 with the Nystrom eigenfunctions
+    e_j(x_ri) = sqrt(sigma_j) V_ij of Section 4; k(x, x) = 1)."""
+    k = V.shape[1]
+    if k == 0:
+        return 1.0
+    w = sigma[:k] - sigma[k]
+    return float(np.max(1.0 - (V * V) @ w))
+
+
+def setup(X, kernel, bandwidth, s, k, sub_idx):
+    """Algorithm 1 initialisation + Section 4 + Section 3 Steps 2-3."""
+    n = X.shape[0]
+    r = np.asarray(sub_idx, dtype=np.int64)
+    if r.shape != (s,) or not (0 <= k < s <= n):
+        raise ValueError("need 0 <= k < s <= n and s subsample indices")
+    Xs = _f64(X[r])
+    Ks = kernel_matrix(Xs, Xs, kernel, bandwidth)
+    # top k+1 eigenpairs of K_s (ascending from LAPACK, reversed)
+    w, U = scipy.linalg.eigh(Ks, subset_by_index=[s - k - 1, s - 1])
+    sigma = w[::-1].copy()
+    U = U[:, ::-1]
+    V = U[:, :k].copy()
+    D = (1.0 - sigma[k] / sigma[:k]) / sigma[:k]
+    beta = beta_closed_form(sigma, V)
+    lam = sigma[k] / s
+    m_star = beta / lam
+    m = int(min(n, max(1, np.floor(m_star))))
+    return OracleState(X, kernel, float(bandwidth), r, Xs, sigma, V, D,
+                       float(beta), float(lam), float(m_star), m)
+
+
+def step_coefficient(beta, lam, m_b):
+    """Per-coordinate step c(m) = 1 / (beta + (m - 1) lambda)."""
+    return 1.0 / (beta + (m_b - 1) * lam)
+
+
+def step(state, alpha, t, y_b, block=_BLOCK):
+    """One iteration of Algorithm 1 (steps 1-5) from weights ``alpha``.
+
+    Returns (alpha_next, F) with F the batch predictions before the update.
+    """
+    t = np.asarray(t, dtype=np.int64)
+    alpha = _f64(alpha)
+    y_b = _f64(y_b)
+    Xb = _f64(state.X[t])
+    # step 2: f(x_tj) = sum_i alpha_i k(x_i, x_tj)
+    F = _kernel_times(Xb, state.X, alpha, state.kernel, state.bandwidth, block)
+    R = F - y_b
+    c = step_coefficient(state.beta, state.lam, t.shape[0])
+    # steps 4-5: sum_i (f(x_ti) - y_ti) V D V^T phi(x_ti)
+    G = kernel_matrix(state.Xs, Xb, state.kernel, state.bandwidth) @ R
+    H = state.V @ (state.D[:, None] * (state.V.T @ G))
+    out = alpha.copy()
+    out[t] -= c * R                 # step 3
+    out[state.r] += c * H           # step 5
+    return out, F
+
+
+def step_pointwise(state, alpha, t, y_b):
+    """Algorithm 1 steps 2-5 one point / one coordinate at a time (tiny
+    inputs only)."""
+    X = _f64(state.X)
+    alpha = _f64(alpha)
+    y_b = _f64(y_b)
+    n, l = alpha.shape
+    m = len(t)
+
+    def k(a, b):
+        diff = a - b
+        d2 = float(np.dot(diff, diff))
+        if state.kernel == GAUSSIAN:
+            return np.exp(-d2 / (2.0 * state.bandwidth ** 2))
+        return np.exp(-np.sqrt(d2) / state.bandwidth)
+
+    f = np.zeros((m, l))
+    for j in range(m):
+        for i in range(n):
+            f[j] += alpha[i] * k(X[i], X[t[j]])
+    c = step_coefficient(state.beta, state.lam, m)
+    out = alpha.copy()
+    for j in range(m):
+        out[t[j]] -= c * (f[j] - y_b[j])
+    # V D V^T as an explicit s x s matrix
+    P = np.zeros((state.s, state.s))
+    for q in range(state.k):
+        P += state.D[q] * np.outer(state.V[:, q], state.V[:, q])
+    for j in range(m):
+        phi = np.array([k(X[state.r[a]], X[t[j]]) for a in range(state.s)])
+        upd = P @ phi
+        for a in range(state.s):
+            out[state.r[a]] += c * (f[j] - y_b[j]) * upd[a]
+    return out, f
+
+
+def predict(X, alpha, Z, kernel, bandwidth, block=_BLOCK):
+    """f(z) = sum_i alpha_i k(x_i, z) for every row z of Z."""
+    return _kernel_times(Z, X, _f64(alpha), kernel, bandwidth, block)
+
+
+def run_epoch(state, alpha, batches, y_of):
+    """Apply ``step`` over a list of index batches; ``y_of(t)`` gives the
+    labels of a batch."""
+    for t in batches:
+        alpha, _ = step(state, alpha, t, y_of(t))
+    return alpha
+
+
+def interpolant(X, Y, kernel, bandwidth):
+    """alpha* = K^{-1} Y (Section 2), by a dense solve."""
+    K = kernel_matrix(X, X, kernel, bandwidth)
+    return np.linalg.solve(K, _f64(Y))
