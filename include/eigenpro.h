@@ -1,0 +1,163 @@
+/*
+ * eigenpro.h — C ABI of libeigenpro, an MI355X (gfx950) implementation of
+ * one EigenPro 2.0 iteration (Ma & Belkin, "Kernel machines that adapt to
+ * GPUs for effective large batch training", arXiv 1806.06144).
+ *
+ * Conventions shared by every call
+ *   - Matrices are row-major float32 unless stated; "device" pointers are
+ *     HIP device memory on the device that was current at ep_setup.
+ *   - All work is enqueued on the stream given to ep_setup and is
+ *     asynchronous unless stated. Device buffers passed in are borrowed for
+ *     the duration of the call's device work: keep them alive until ep_sync
+ *     (or a stream synchronisation) returns.
+ *   - Return value: EP_OK (0) or a negative EP_E* code. The text of the last
+ *     error of the calling thread is available from ep_last_error(). No C++
+ *     exception crosses this boundary.
+ *   - A context is not thread-safe: calls on one context must not overlap.
+ *     Different contexts are independent.
+ */
+#ifndef EIGENPRO_H
+#define EIGENPRO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    EP_OK = 0,
+    EP_EINVAL = -1,    /* an argument is out of its documented range        */
+    EP_ENOMEM = -2,    /* a device or host allocation failed                 */
+    EP_EDEVICE = -3,   /* a HIP / rocSOLVER call failed                      */
+    EP_ENUMERIC = -4,  /* eigensolve failed or sigma_{k+1} <= 0              */
+    EP_EINDEX = -5     /* a batch index was out of range or repeated         */
+};
+
+enum {
+    EP_GAUSSIAN = 0,   /* k(x,z) = exp(-|x-z|^2 / (2 bw^2))  (Appendix B)    */
+    EP_LAPLACIAN = 1   /* k(x,z) = exp(-|x-z| / bw)          (Appendix B)    */
+};
+
+typedef struct ep_ctx ep_ctx;
+
+/* Products of setup (Algorithm 1 initialisation; Sections 3 and 4). */
+typedef struct ep_info {
+    int64_t n, d, l, s, k;
+    double sigma_1;     /* largest eigenvalue of K_s                          */
+    double sigma_k1;    /* sigma_{k+1}: level the top k eigenvalues flatten to */
+    double lambda_k1;   /* sigma_{k+1} / s: top eigenvalue of the adapted
+                           operator (Nystrom, Section 4)                      */
+    double beta;        /* beta(K_G): max of k_G(x,x) over the s subsample
+                           points (Section 3, Step 2)                         */
+    double m_star;      /* beta / lambda_k1: critical batch of the adapted
+                           kernel (Section 2)                                 */
+    int64_t m;          /* min(n, max(1, floor(m_star)))                       */
+    double eta;         /* m / (beta + (m-1) lambda_k1): step size at m; one
+                           step moves each coordinate by eta/m times its
+                           residual                                          */
+    double setup_ms;    /* wall time of ep_setup                              */
+} ep_info;
+
+/*
+ * ep_setup — Algorithm 1 initialisation, Section 4 (Nystrom extension) and
+ * Section 3 Steps 2-3 (beta, critical batch, step size).
+ *
+ *   ctx        out: new context (NULL on failure).
+ *   X          device, n x d, row-major float32 training features (the
+ *              kernel centres). BORROWED: never copied, must stay alive and
+ *              unchanged until ep_destroy.
+ *   n, d, l    centres, feature dimension, label columns; each >= 1.
+ *   kernel     EP_GAUSSIAN or EP_LAPLACIAN; bandwidth > 0 and finite.
+ *   s, k       subsample size and preconditioner rank, 0 <= k < s <= n.
+ *              The top k+1 eigenpairs of K_s = [k(x_ri, x_rj)] are computed;
+ *              the top k directions are flattened to sigma_{k+1}.
+ *   sub_idx    host, s distinct indices in [0, n), or NULL to draw s
+ *              indices uniformly without replacement from `seed`.
+ *   hip_stream hipStream_t to enqueue all work on (NULL = default stream).
+ *   info       out (may be NULL): see ep_info.
+ * Sets alpha = 0. Blocks until setup is complete. K_s is formed in float64;
+ * the eigensolve runs on the device in float64.
+ * Errors: EP_EINVAL (ranges above, duplicate/out-of-range sub_idx),
+ * EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC.
+ */
+int ep_setup(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
+             int kernel, float bandwidth, int64_t s, int64_t k,
+             const int64_t* sub_idx, uint64_t seed, void* hip_stream,
+             ep_info* info);
+
+/*
+ * ep_step — one iteration of Algorithm 1 (steps 1-5) on a batch of m points.
+ *
+ *   t       device int64[m]: batch indices, distinct, in [0, n).
+ *   m       1 <= m <= n. The step coefficient is 1/(beta + (m-1) lambda_k1)
+ *           for this call's m, so a short last batch is handled.
+ *   y_b     device float32 m x l: labels of the batch rows.
+ *   f_out   device float32 m x l or NULL: receives f(x_t) before the update.
+ * Computes F = K(X_t, X) alpha, R = F - y_b, updates alpha_t -= c R and
+ * alpha_r += c V D V^T K(X_r, X_t) R with D_i = (1 - sigma_{k+1}/sigma_i) /
+ * sigma_i. Asynchronous. Indices outside [0, n) are not read or written
+ * and make the next ep_sync return EP_EINDEX; repeated indices are
+ * rejected with EP_EINDEX only when index checking is enabled
+ * (ep_set_checks), since that check copies t to the host and synchronises.
+ * Errors: EP_EINVAL (m out of range, NULL t / y_b), EP_EINDEX, EP_ENOMEM,
+ * EP_EDEVICE.
+ */
+int ep_step(ep_ctx* ctx, const int64_t* t, int64_t m, const float* y_b,
+            float* f_out);
+
+/*
+ * ep_predict — f(z) = sum_i alpha_i k(x_i, z) (Section 2) for each row z.
+ *   Z    device float32 n_z x d.   out  device float32 n_z x l.
+ * n_z >= 0 (0 is a no-op). Asynchronous.
+ */
+int ep_predict(ep_ctx* ctx, const float* Z, int64_t n_z, float* out);
+
+/* alpha as a dense n x l float32 device matrix (copy out / copy in).
+ * Asynchronous on the context stream. */
+int ep_get_alpha(ep_ctx* ctx, float* out);
+int ep_set_alpha(ep_ctx* ctx, const float* in);
+
+/* Setup products for inspection (host buffers; blocking):
+ *   sigma  double[k+1] descending eigenvalues of K_s (may be NULL)
+ *   D      double[k] preconditioner scales (may be NULL)
+ *   V      float[s*k] row-major top-k eigenvectors, row i for r_i (may be NULL)
+ *   r      int64[s] subsample indices (may be NULL) */
+int ep_get_preconditioner(ep_ctx* ctx, double* sigma, double* D, float* V,
+                          int64_t* r);
+
+int ep_get_info(ep_ctx* ctx, ep_info* info);
+
+/* Enable (1) / disable (0, default) host-side validation of batch indices
+ * in ep_step (copies t to the host and synchronises). */
+int ep_set_checks(ep_ctx* ctx, int on);
+
+/* Timing of the dominant kernel (the fused kernel-block contraction of
+ * step 2) and of whole steps, by HIP events on the context stream.
+ * ep_timing_enable(ctx, 1) starts recording and clears totals;
+ * ep_timing_read synchronises the stream and returns the totals in ms. */
+typedef struct ep_timing {
+    double kmv_ms;          /* sum over launches of the step-2 kernel */
+    int64_t kmv_launches;
+    double step_ms;         /* sum over ep_step calls */
+    int64_t steps;
+} ep_timing;
+int ep_timing_enable(ep_ctx* ctx, int on);
+int ep_timing_read(ep_ctx* ctx, ep_timing* out);
+
+/* Wait for all work of the context; reports deferred device errors
+ * (EP_EDEVICE) and out-of-range batch indices seen since the last call
+ * (EP_EINDEX). */
+int ep_sync(ep_ctx* ctx);
+
+/* Free the context and everything it owns (not X). NULL is a no-op. */
+void ep_destroy(ep_ctx* ctx);
+
+/* Message for the calling thread's last error ("" if none). */
+const char* ep_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EIGENPRO_H */

@@ -1,0 +1,214 @@
+"""Python binding of libeigenpro: argument marshalling over the C ABI only.
+
+Every function has the name and meaning of its C counterpart in
+``include/eigenpro.h``; device arguments may be torch tensors (checked for
+dtype, device and contiguity, then passed by pointer) or raw integer device
+addresses. All computation happens in the HIP library: if ``libeigenpro.so``
+is missing this module raises at import, it never falls back.
+"""
+
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeigenpro.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "eigenpro.h")
+
+EP_OK, EP_EINVAL, EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC, EP_EINDEX = 0, -1, -2, -3, -4, -5
+EP_GAUSSIAN, EP_LAPLACIAN = 0, 1
+KERNELS = {"gaussian": EP_GAUSSIAN, "laplacian": EP_LAPLACIAN}
+_CODES = {EP_EINVAL: "EP_EINVAL", EP_ENOMEM: "EP_ENOMEM", EP_EDEVICE: "EP_EDEVICE",
+          EP_ENUMERIC: "EP_ENUMERIC", EP_EINDEX: "EP_EINDEX"}
+
+
+class EpInfo(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int64), ("l", ctypes.c_int64),
+                ("s", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("sigma_1", ctypes.c_double), ("sigma_k1", ctypes.c_double),
+                ("lambda_k1", ctypes.c_double), ("beta", ctypes.c_double),
+                ("m_star", ctypes.c_double), ("m", ctypes.c_int64),
+                ("eta", ctypes.c_double), ("setup_ms", ctypes.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class EpTiming(ctypes.Structure):
+    _fields_ = [("kmv_ms", ctypes.c_double), ("kmv_launches", ctypes.c_int64),
+                ("step_ms", ctypes.c_double), ("steps", ctypes.c_int64)]
+
+
+class EigenProError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{_CODES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "or python -m paper_1806_06144_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    sig = {
+        "ep_setup": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P,
+                         ctypes.c_uint64, P, ctypes.POINTER(EpInfo)]),
+        "ep_step": (I, [P, P, I64, P, P]),
+        "ep_predict": (I, [P, P, I64, P]),
+        "ep_get_alpha": (I, [P, P]),
+        "ep_set_alpha": (I, [P, P]),
+        "ep_get_preconditioner": (I, [P, P, P, P, P]),
+        "ep_get_info": (I, [P, ctypes.POINTER(EpInfo)]),
+        "ep_set_checks": (I, [P, I]),
+        "ep_timing_enable": (I, [P, I]),
+        "ep_timing_read": (I, [P, ctypes.POINTER(EpTiming)]),
+        "ep_sync": (I, [P]),
+        "ep_destroy": (None, [P]),
+        "ep_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def declared_symbols():
+    """Names of the functions declared in include/eigenpro.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ep_[a-z_0-9]+)\s*\(", text)))
+
+
+def _check(rc):
+    if rc != EP_OK:
+        raise EigenProError(rc, _lib.ep_last_error().decode())
+    return rc
+
+
+def _ptr(x, dtype=None, allow_none=False):
+    """Device address of a tensor (validated) or an integer address."""
+    if x is None:
+        if allow_none:
+            return None
+        raise ValueError("a device buffer is required")
+    if isinstance(x, int):
+        return x
+    if not x.is_cuda:
+        raise ValueError("expected a device tensor")
+    if dtype is not None and x.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {x.dtype}")
+    if not x.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return x.data_ptr()
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream):
+    if stream is None:
+        return _torch().cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def ep_last_error():
+    return _lib.ep_last_error().decode()
+
+
+def ep_setup(X, n, d, l, kernel, bandwidth, s, k, sub_idx=None, seed=0, stream=None):
+    """Returns (ctx, EpInfo). X: device float32 n x d (borrowed: keep it
+    alive until ep_destroy). sub_idx: host int64 sequence of s indices or
+    None."""
+    torch = _torch()
+    if isinstance(kernel, str):
+        kernel = KERNELS[kernel]
+    xp = _ptr(X, torch.float32)
+    sub_ptr = None
+    keep = None
+    if sub_idx is not None:
+        import numpy as np
+        keep = np.ascontiguousarray(np.asarray(sub_idx, dtype=np.int64))
+        if keep.shape != (s,):
+            raise ValueError("sub_idx must hold s indices")
+        sub_ptr = keep.ctypes.data
+    ctx = ctypes.c_void_p()
+    info = EpInfo()
+    _check(_lib.ep_setup(ctypes.byref(ctx), xp, n, d, l, kernel, bandwidth, s, k, sub_ptr,
+                         seed, _stream_handle(stream), ctypes.byref(info)))
+    return ctx, info
+
+
+def ep_step(ctx, t, m, y_b, f_out=None):
+    torch = _torch()
+    return _check(_lib.ep_step(ctx, _ptr(t, torch.int64), m, _ptr(y_b, torch.float32),
+                               _ptr(f_out, torch.float32, allow_none=True)))
+
+
+def ep_predict(ctx, Z, n_z, out):
+    torch = _torch()
+    return _check(_lib.ep_predict(ctx, _ptr(Z, torch.float32), n_z, _ptr(out, torch.float32)))
+
+
+def ep_get_alpha(ctx, out):
+    return _check(_lib.ep_get_alpha(ctx, _ptr(out, _torch().float32)))
+
+
+def ep_set_alpha(ctx, alpha):
+    return _check(_lib.ep_set_alpha(ctx, _ptr(alpha, _torch().float32)))
+
+
+def ep_get_preconditioner(ctx, info):
+    """Returns numpy (sigma[k+1], D[k], V[s, k] float32, r[s])."""
+    import numpy as np
+    k, s = info.k, info.s
+    sigma = np.zeros(k + 1, dtype=np.float64)
+    D = np.zeros(max(k, 1), dtype=np.float64)
+    V = np.zeros((s, max(k, 1)), dtype=np.float32)
+    r = np.zeros(s, dtype=np.int64)
+    _check(_lib.ep_get_preconditioner(ctx, sigma.ctypes.data, D.ctypes.data, V.ctypes.data,
+                                      r.ctypes.data))
+    return sigma, D[:k], V[:, :k], r
+
+
+def ep_get_info(ctx):
+    info = EpInfo()
+    _check(_lib.ep_get_info(ctx, ctypes.byref(info)))
+    return info
+
+
+def ep_set_checks(ctx, on):
+    return _check(_lib.ep_set_checks(ctx, 1 if on else 0))
+
+
+def ep_timing_enable(ctx, on):
+    return _check(_lib.ep_timing_enable(ctx, 1 if on else 0))
+
+
+def ep_timing_read(ctx):
+    t = EpTiming()
+    _check(_lib.ep_timing_read(ctx, ctypes.byref(t)))
+    return t
+
+
+def ep_sync(ctx):
+    return _check(_lib.ep_sync(ctx))
+
+
+def ep_destroy(ctx):
+    _lib.ep_destroy(ctx)
+
+
+def raw_call(name, *args):
+    """Call a C entry point with already-marshalled arguments and return its
+    integer status (used to exercise error paths)."""
+    return getattr(_lib, name)(*args)

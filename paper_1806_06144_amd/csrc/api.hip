@@ -1,0 +1,602 @@
+// C ABI of libeigenpro: context, argument checking, buffer management and the
+// launch sequence of one EigenPro 2.0 iteration (Algorithm 1) on one GPU.
+#include "../../include/eigenpro.h"
+#include "ep_internal.h"
+
+#include <rocblas/rocblas.h>
+#include <rocsolver/rocsolver.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace ep;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (expr);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return fail(e_ == hipErrorOutOfMemory ? EP_ENOMEM : EP_EDEVICE, "%s: %s (%s)", \
+                        #expr, hipGetErrorString(e_), __func__);                       \
+    } while (0)
+
+// Grow-only device buffer.
+struct DevBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+    hipError_t ensure(size_t want) {
+        if (want <= bytes) return hipSuccess;
+        if (p) {
+            hipError_t e = hipFree(p);
+            if (e != hipSuccess) return e;
+            p = nullptr;
+            bytes = 0;
+        }
+        hipError_t e = hipMalloc(&p, std::max<size_t>(want, 256));
+        if (e == hipSuccess) bytes = want;
+        return e;
+    }
+    void release() {
+        if (p) (void)hipFree(p);
+        p = nullptr;
+        bytes = 0;
+    }
+    template <class T>
+    T* as() const {
+        return static_cast<T*>(p);
+    }
+};
+
+struct TimedPair {
+    hipEvent_t a, b;
+};
+
+uint64_t splitmix64(uint64_t& x) {
+    uint64_t z = (x += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+}  // namespace
+
+struct ep_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    const float* X = nullptr;
+    int64_t n = 0, d = 0, l = 0, s = 0, k = 0;
+    int kind = 0;
+    float bandwidth = 1.f;
+    float scale = 0.f;
+    int64_t l_pad = 0, n_pad = 0, s_pad = 0, k_ld = 1;
+    ep_info info{};
+    std::vector<double> sigma, D;
+    std::vector<int64_t> r_host;
+    bool checks = false;
+    std::vector<unsigned char> seen;
+
+    DevBuf norms, alpha, r_dev, Xs, xs_norms, V, Dk, err;
+    // per-call scratch
+    DevBuf xb, xb_norms, R, part, G, vt_part, W1, zn;
+
+    bool timing = false;
+    std::vector<TimedPair> kmv_ev, step_ev;
+    ep_timing tsum{};
+
+    ~ep_ctx() {
+        for (DevBuf* b : {&norms, &alpha, &r_dev, &Xs, &xs_norms, &V, &Dk, &err, &xb, &xb_norms,
+                          &R, &part, &G, &vt_part, &W1, &zn})
+            b->release();
+        for (auto& p : kmv_ev) {
+            (void)hipEventDestroy(p.a);
+            (void)hipEventDestroy(p.b);
+        }
+        for (auto& p : step_ev) {
+            (void)hipEventDestroy(p.a);
+            (void)hipEventDestroy(p.b);
+        }
+    }
+};
+
+namespace {
+
+constexpr size_t kPartBudget = size_t(2) << 30;   // bytes of split partial sums
+
+int max_slices_for(int64_t rows_pad, int64_t ldw) {
+    const size_t per = (size_t)rows_pad * (size_t)ldw * sizeof(float);
+    return (int)std::max<size_t>(1, std::min<size_t>(256, kPartBudget / std::max<size_t>(per, 1)));
+}
+
+int record(hipStream_t s, std::vector<TimedPair>& v, bool start) {
+    if (start) {
+        TimedPair p;
+        HIP_TRY(hipEventCreate(&p.a));
+        HIP_TRY(hipEventCreate(&p.b));
+        v.push_back(p);
+        HIP_TRY(hipEventRecord(v.back().a, s));
+    } else {
+        HIP_TRY(hipEventRecord(v.back().b, s));
+    }
+    return EP_OK;
+}
+
+// sum_j k(q_i, c_j) W_j for all rows of Q: fused kernel + reduction target
+// is the caller's; returns the slice count in *slices.
+int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
+            int64_t nq, const float* C, int64_t ldc, const float* cn, const int64_t* cid,
+            int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed) {
+    *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
+    KmvPlan plan = kmv_plan(nq, nc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
+    *slices = plan.slices();
+    HIP_TRY(c->part.ensure((size_t)plan.slices() * (size_t)(*rows_pad) * c->l_pad * sizeof(float)));
+    KmvArgs a{};
+    a.Q = Q;
+    a.ldq = ldq;
+    a.qn = qn;
+    a.qid = qid;
+    a.nq = nq;
+    a.C = C;
+    a.ldc = ldc;
+    a.cn = cn;
+    a.cid = cid;
+    a.nc = nc;
+    a.d = c->d;
+    a.W = W;
+    a.ldw = c->l_pad;
+    a.lt = (int)(c->l_pad / kTile);
+    a.out = c->part.as<float>();
+    a.out_rows = *rows_pad;
+    a.kind = c->kind;
+    a.scale = c->scale;
+    if (timed) {
+        int rc = record(c->stream, c->kmv_ev, true);
+        if (rc) return rc;
+    }
+    HIP_TRY(kmv_launch(a, plan, c->stream));
+    if (timed) {
+        int rc = record(c->stream, c->kmv_ev, false);
+        if (rc) return rc;
+    }
+    return EP_OK;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) (void)hipSetDevice(dev);
+        else prev = -1;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
+    const int64_t n = c->n, d = c->d, s = c->s, k = c->k;
+    hipStream_t st = c->stream;
+
+    // subsample indices (Algorithm 1: fixed coordinate block r)
+    c->r_host.resize(s);
+    if (sub_idx) {
+        std::vector<unsigned char> seen(n, 0);
+        for (int64_t i = 0; i < s; ++i) {
+            const int64_t v = sub_idx[i];
+            if (v < 0 || v >= n) return fail(EP_EINVAL, "sub_idx[%lld]=%lld outside [0,%lld)",
+                                             (long long)i, (long long)v, (long long)n);
+            if (seen[v]) return fail(EP_EINVAL, "sub_idx repeats index %lld", (long long)v);
+            seen[v] = 1;
+            c->r_host[i] = v;
+        }
+    } else {
+        std::vector<int64_t> perm(n);
+        for (int64_t i = 0; i < n; ++i) perm[i] = i;
+        uint64_t st_rng = seed;
+        for (int64_t i = 0; i < s; ++i) {
+            const uint64_t span = (uint64_t)(n - i);
+            const int64_t j = i + (int64_t)(splitmix64(st_rng) % span);
+            std::swap(perm[i], perm[j]);
+            c->r_host[i] = perm[i];
+        }
+    }
+
+    c->l_pad = round_up(c->l, kTile);
+    c->n_pad = round_up(n, kBN);
+    c->s_pad = round_up(s, kBM);
+    c->k_ld = std::max<int64_t>(k, 1);
+
+    HIP_TRY(c->err.ensure(sizeof(int)));
+    HIP_TRY(hipMemsetAsync(c->err.p, 0, sizeof(int), st));
+    HIP_TRY(c->norms.ensure((size_t)c->n_pad * sizeof(float)));
+    HIP_TRY(c->alpha.ensure((size_t)c->n_pad * c->l_pad * sizeof(float)));
+    HIP_TRY(c->r_dev.ensure((size_t)s * sizeof(int64_t)));
+    HIP_TRY(c->Xs.ensure((size_t)c->s_pad * d * sizeof(float)));
+    HIP_TRY(c->xs_norms.ensure((size_t)c->s_pad * sizeof(float)));
+    HIP_TRY(c->V.ensure((size_t)s * c->k_ld * sizeof(float)));
+    HIP_TRY(c->Dk.ensure((size_t)c->k_ld * sizeof(float)));
+
+    HIP_TRY(launch_fill_f32(c->alpha.as<float>(), c->n_pad * c->l_pad, 0.f, st));
+    HIP_TRY(launch_fill_f32(c->norms.as<float>(), c->n_pad, 0.f, st));
+    HIP_TRY(hipMemcpyAsync(c->r_dev.p, c->r_host.data(), s * sizeof(int64_t),
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_row_norms(c->X, n, d, d, c->norms.as<float>(), st));
+    HIP_TRY(launch_gather_rows(c->X, n, d, c->norms.as<float>(), c->r_dev.as<int64_t>(), s,
+                               c->s_pad, c->Xs.as<float>(), c->xs_norms.as<float>(),
+                               c->err.as<int>(), st));
+
+    // K_s in float64 and its top k+1 eigenpairs (Algorithm 1 initialisation)
+    DevBuf Ks, Z, W, kp, sig_dev, iinfo;
+    struct Free {
+        DevBuf* b[5];
+        ~Free() {
+            for (DevBuf* x : b) x->release();
+        }
+    } guard{{&Ks, &Z, &W, &kp, &sig_dev}};
+    HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
+    HIP_TRY(Z.ensure((size_t)s * s * sizeof(double)));
+    HIP_TRY(W.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
+    HIP_TRY(iinfo.ensure(2 * sizeof(rocblas_int)));
+    HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
+                                        Ks.as<double>(), st));
+
+    rocblas_handle h = nullptr;
+    if (rocblas_create_handle(&h) != rocblas_status_success) {
+        iinfo.release();
+        return fail(EP_EDEVICE, "rocblas_create_handle failed");
+    }
+    rocblas_set_stream(h, st);
+    rocblas_int* dinfo = iinfo.as<rocblas_int>();
+    const rocblas_status rs = rocsolver_dsyevdx(
+        h, rocblas_evect_original, rocblas_erange_index, rocblas_fill_upper, (rocblas_int)s,
+        Ks.as<double>(), (rocblas_int)s, 0.0, 0.0, (rocblas_int)(s - k), (rocblas_int)s, dinfo,
+        W.as<double>(), Z.as<double>(), (rocblas_int)s, dinfo + 1);
+    rocblas_destroy_handle(h);
+    if (rs != rocblas_status_success) {
+        iinfo.release();
+        return fail(EP_EDEVICE, "rocsolver_dsyevdx returned status %d", (int)rs);
+    }
+    rocblas_int hinfo[2] = {0, 0};
+    std::vector<double> w_asc(k + 1);
+    HIP_TRY(hipMemcpyAsync(hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.p, (k + 1) * sizeof(double), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    iinfo.release();
+    if (hinfo[1] != 0 || hinfo[0] != (rocblas_int)(k + 1))
+        return fail(EP_ENUMERIC, "eigensolve failed: info=%d, found %d of %lld eigenpairs",
+                    (int)hinfo[1], (int)hinfo[0], (long long)(k + 1));
+    c->sigma.assign(w_asc.rbegin(), w_asc.rend());
+    if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
+        return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
+
+    // D_i = (1 - sigma_{k+1}/sigma_i) / sigma_i (Section 4, Eq. 8 with q = k+1)
+    c->D.resize(k);
+    std::vector<float> dk(c->k_ld, 0.f);
+    for (int64_t i = 0; i < k; ++i) {
+        c->D[i] = (1.0 - c->sigma[k] / c->sigma[i]) / c->sigma[i];
+        dk[i] = (float)c->D[i];
+    }
+    HIP_TRY(hipMemcpyAsync(c->Dk.p, dk.data(), c->k_ld * sizeof(float), hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_extract_eigvecs(Z.as<double>(), s, s, k, sig_dev.as<double>(), c->V.as<float>(),
+                                   c->k_ld, kp.as<double>(), st));
+    std::vector<double> kpd(s);
+    HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
+    int herr = 0;
+    HIP_TRY(hipMemcpyAsync(&herr, c->err.p, sizeof(int), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    if (herr) return fail(EP_EINVAL, "subsample index out of range");
+
+    // Section 3 Step 2: beta(K_G) over the subsample points; lambda_1(K_G) =
+    // sigma_{k+1}/s; Section 2: m* = beta / lambda_1; Step 3: batch and step.
+    double beta = -1e300;
+    for (double v : kpd) beta = std::max(beta, v);
+    if (k == 0) beta = 1.0;
+    const double lam = c->sigma[k] / (double)s;
+    const double m_star = beta / lam;
+    const int64_t m = std::min<int64_t>(n, std::max<int64_t>(1, (int64_t)std::floor(m_star)));
+
+    ep_info& I = c->info;
+    I.n = n;
+    I.d = d;
+    I.l = c->l;
+    I.s = s;
+    I.k = k;
+    I.sigma_1 = c->sigma[0];
+    I.sigma_k1 = c->sigma[k];
+    I.lambda_k1 = lam;
+    I.beta = beta;
+    I.m_star = m_star;
+    I.m = m;
+    I.eta = (double)m / (beta + (double)(m - 1) * lam);
+    return EP_OK;
+}
+
+int ensure_step_buffers(ep_ctx* c, int64_t m) {
+    const int64_t m_pad = round_up(m, kBN);
+    HIP_TRY(c->xb.ensure((size_t)m_pad * c->d * sizeof(float)));
+    HIP_TRY(c->xb_norms.ensure((size_t)m_pad * sizeof(float)));
+    HIP_TRY(c->R.ensure((size_t)m_pad * c->l_pad * sizeof(float)));
+    return EP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ep_last_error(void) { return g_err.c_str(); }
+
+int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
+             float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
+             void* hip_stream, ep_info* info) {
+    g_err.clear();
+    if (!out) return fail(EP_EINVAL, "ctx out-pointer is NULL");
+    *out = nullptr;
+    if (!X) return fail(EP_EINVAL, "X is NULL");
+    if (n < 1 || d < 1 || l < 1) return fail(EP_EINVAL, "need n, d, l >= 1");
+    if (!(0 <= k && k < s && s <= n)) return fail(EP_EINVAL, "need 0 <= k < s <= n");
+    if (kernel != EP_GAUSSIAN && kernel != EP_LAPLACIAN)
+        return fail(EP_EINVAL, "unknown kernel id %d", kernel);
+    if (!(bandwidth > 0.f) || !std::isfinite(bandwidth))
+        return fail(EP_EINVAL, "bandwidth must be positive and finite");
+    if (s > 46340) return fail(EP_EINVAL, "s = %lld exceeds the eigensolver's 32-bit index range",
+                               (long long)s);
+    const auto t0 = std::chrono::steady_clock::now();
+    ep_ctx* c = new (std::nothrow) ep_ctx();
+    if (!c) return fail(EP_ENOMEM, "host allocation failed");
+    if (hipGetDevice(&c->device) != hipSuccess) {
+        delete c;
+        return fail(EP_EDEVICE, "no HIP device");
+    }
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    c->X = X;
+    c->n = n;
+    c->d = d;
+    c->l = l;
+    c->s = s;
+    c->k = k;
+    c->kind = kernel;
+    c->bandwidth = bandwidth;
+    c->scale = kernel_scale(kernel, bandwidth);
+    const int rc = do_setup(c, sub_idx, seed);
+    if (rc != EP_OK) {
+        (void)hipStreamSynchronize(c->stream);
+        delete c;
+        return rc;
+    }
+    c->info.setup_ms =
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    if (info) *info = c->info;
+    *out = c;
+    return EP_OK;
+}
+
+int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_out) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (!t || !y_b) return fail(EP_EINVAL, "t and y_b must be device pointers");
+    if (m < 1 || m > c->n) return fail(EP_EINVAL, "batch size m=%lld outside [1, n]", (long long)m);
+    DeviceGuard dg(c->device);
+    hipStream_t st = c->stream;
+    if (c->checks) {
+        std::vector<int64_t> th(m);
+        HIP_TRY(hipMemcpyAsync(th.data(), t, m * sizeof(int64_t), hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipStreamSynchronize(st));
+        c->seen.assign(c->n, 0);
+        for (int64_t i = 0; i < m; ++i) {
+            if (th[i] < 0 || th[i] >= c->n)
+                return fail(EP_EINDEX, "t[%lld]=%lld outside [0,%lld)", (long long)i,
+                            (long long)th[i], (long long)c->n);
+            if (c->seen[th[i]]) return fail(EP_EINDEX, "t repeats index %lld", (long long)th[i]);
+            c->seen[th[i]] = 1;
+        }
+    }
+    int rc = ensure_step_buffers(c, m);
+    if (rc) return rc;
+    if (c->timing) {
+        rc = record(st, c->step_ev, true);
+        if (rc) return rc;
+    }
+    const int64_t m_pad = round_up(m, kBN);
+    float* xb = c->xb.as<float>();
+    float* xbn = c->xb_norms.as<float>();
+    float* alpha = c->alpha.as<float>();
+    float* R = c->R.as<float>();
+
+    // step 1: gather the batch
+    HIP_TRY(launch_gather_rows(c->X, c->n, c->d, c->norms.as<float>(), t, m, m_pad, xb, xbn,
+                               c->err.as<int>(), st));
+    // step 2: F = K(X_t, X) alpha, fused
+    int slices = 0;
+    int64_t rows_pad = 0;
+    rc = run_kmv(c, xb, c->d, xbn, t, m, c->X, c->d, c->norms.as<float>(), nullptr, c->n, alpha,
+                 &slices, &rows_pad, c->timing);
+    if (rc) return rc;
+    // step 3: R = F - y_b; alpha_t -= c R
+    const double coef = 1.0 / (c->info.beta + (double)(m - 1) * c->info.lambda_k1);
+    HIP_TRY(launch_reduce_residual(c->part.as<float>(), slices, rows_pad, c->l_pad, m, c->l, y_b,
+                                   f_out, R, alpha, c->n, t, (float)coef, st));
+    if (c->k > 0) {
+        // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
+        rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(), c->r_dev.as<int64_t>(),
+                     c->s, xb, c->d, xbn, t, m, R, &slices, &rows_pad, false);
+        if (rc) return rc;
+        HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
+        HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s, c->l_pad,
+                                   c->G.as<float>(), c->l_pad, st));
+        const int64_t per_slice = ceil_div(c->l_pad, 64) * ceil_div(c->k, 64);
+        const int vs = (int)std::max<int64_t>(
+            1, std::min<int64_t>(512 / std::max<int64_t>(per_slice, 1), ceil_div(c->s, 64)));
+        HIP_TRY(c->vt_part.ensure((size_t)vs * round_up(c->k, 64) * c->l_pad * sizeof(float)));
+        HIP_TRY(c->W1.ensure((size_t)c->k * c->l_pad * sizeof(float)));
+        HIP_TRY(launch_vt_g(c->V.as<float>(), c->k_ld, c->G.as<float>(), c->l_pad, c->s, c->k,
+                            c->l_pad, c->vt_part.as<float>(), vs, st));
+        HIP_TRY(launch_reduce_scale(c->vt_part.as<float>(), vs, c->k, c->l_pad, c->Dk.as<float>(),
+                                    c->W1.as<float>(), st));
+        HIP_TRY(launch_lowrank_update(c->V.as<float>(), c->k_ld, c->W1.as<float>(), c->l_pad, c->s,
+                                      c->k, c->l, c->r_dev.as<int64_t>(), alpha, c->l_pad,
+                                      (float)coef, st));
+    }
+    if (c->timing) {
+        rc = record(st, c->step_ev, false);
+        if (rc) return rc;
+    }
+    return EP_OK;
+}
+
+int ep_predict(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (n_z < 0) return fail(EP_EINVAL, "n_z < 0");
+    if (n_z == 0) return EP_OK;
+    if (!Z || !out) return fail(EP_EINVAL, "Z and out must be device pointers");
+    DeviceGuard dg(c->device);
+    hipStream_t st = c->stream;
+    const int64_t chunk = 32768;
+    HIP_TRY(c->zn.ensure((size_t)std::min(n_z, chunk) * sizeof(float)));
+    for (int64_t z0 = 0; z0 < n_z; z0 += chunk) {
+        const int64_t nz = std::min(chunk, n_z - z0);
+        const float* Zc = Z + z0 * c->d;
+        HIP_TRY(launch_row_norms(Zc, nz, c->d, c->d, c->zn.as<float>(), st));
+        int slices = 0;
+        int64_t rows_pad = 0;
+        int rc = run_kmv(c, Zc, c->d, c->zn.as<float>(), nullptr, nz, c->X, c->d,
+                         c->norms.as<float>(), nullptr, c->n, c->alpha.as<float>(), &slices,
+                         &rows_pad, false);
+        if (rc) return rc;
+        HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, nz, c->l,
+                                   out + z0 * c->l, c->l, st));
+    }
+    return EP_OK;
+}
+
+int ep_get_alpha(ep_ctx* c, float* out) {
+    g_err.clear();
+    if (!c || !out) return fail(EP_EINVAL, "NULL argument");
+    DeviceGuard dg(c->device);
+    HIP_TRY(hipMemcpy2DAsync(out, c->l * sizeof(float), c->alpha.p, c->l_pad * sizeof(float),
+                             c->l * sizeof(float), c->n, hipMemcpyDeviceToDevice, c->stream));
+    return EP_OK;
+}
+
+int ep_set_alpha(ep_ctx* c, const float* in) {
+    g_err.clear();
+    if (!c || !in) return fail(EP_EINVAL, "NULL argument");
+    DeviceGuard dg(c->device);
+    HIP_TRY(hipMemcpy2DAsync(c->alpha.p, c->l_pad * sizeof(float), in, c->l * sizeof(float),
+                             c->l * sizeof(float), c->n, hipMemcpyDeviceToDevice, c->stream));
+    return EP_OK;
+}
+
+int ep_get_preconditioner(ep_ctx* c, double* sigma, double* D, float* V, int64_t* r) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    DeviceGuard dg(c->device);
+    if (sigma) std::memcpy(sigma, c->sigma.data(), (c->k + 1) * sizeof(double));
+    if (D && c->k) std::memcpy(D, c->D.data(), c->k * sizeof(double));
+    if (r) std::memcpy(r, c->r_host.data(), c->s * sizeof(int64_t));
+    if (V && c->k) {
+        HIP_TRY(hipMemcpyAsync(V, c->V.p, (size_t)c->s * c->k * sizeof(float),
+                               hipMemcpyDeviceToHost, c->stream));
+        HIP_TRY(hipStreamSynchronize(c->stream));
+    }
+    return EP_OK;
+}
+
+int ep_get_info(ep_ctx* c, ep_info* info) {
+    g_err.clear();
+    if (!c || !info) return fail(EP_EINVAL, "NULL argument");
+    *info = c->info;
+    return EP_OK;
+}
+
+int ep_set_checks(ep_ctx* c, int on) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    c->checks = on != 0;
+    return EP_OK;
+}
+
+int ep_timing_enable(ep_ctx* c, int on) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    DeviceGuard dg(c->device);
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    for (auto* v : {&c->kmv_ev, &c->step_ev}) {
+        for (auto& p : *v) {
+            (void)hipEventDestroy(p.a);
+            (void)hipEventDestroy(p.b);
+        }
+        v->clear();
+    }
+    c->tsum = ep_timing{};
+    c->timing = on != 0;
+    return EP_OK;
+}
+
+int ep_timing_read(ep_ctx* c, ep_timing* out) {
+    g_err.clear();
+    if (!c || !out) return fail(EP_EINVAL, "NULL argument");
+    DeviceGuard dg(c->device);
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    ep_timing t{};
+    for (auto& p : c->kmv_ev) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.a, p.b));
+        t.kmv_ms += ms;
+        t.kmv_launches += 1;
+    }
+    for (auto& p : c->step_ev) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.a, p.b));
+        t.step_ms += ms;
+        t.steps += 1;
+    }
+    *out = t;
+    return EP_OK;
+}
+
+int ep_sync(ep_ctx* c) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    DeviceGuard dg(c->device);
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    int herr = 0;
+    HIP_TRY(hipMemcpy(&herr, c->err.p, sizeof(int), hipMemcpyDeviceToHost));
+    if (herr) {
+        HIP_TRY(hipMemset(c->err.p, 0, sizeof(int)));
+        return fail(EP_EINDEX, "a batch index was outside [0, n)");
+    }
+    return EP_OK;
+}
+
+void ep_destroy(ep_ctx* c) {
+    if (!c) return;
+    DeviceGuard dg(c->device);
+    (void)hipStreamSynchronize(c->stream);
+    delete c;
+}
+
+}  // extern "C"

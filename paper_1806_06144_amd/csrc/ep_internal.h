@@ -1,0 +1,91 @@
+// Internal interfaces of libeigenpro (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ep {
+
+// Tile geometry of the fused kernel-block contraction (kmv.hip).
+constexpr int kTile = 32;                 // MFMA 32x32 output tile edge
+constexpr int kQSub = 2;                  // query sub-tiles per workgroup
+constexpr int kCSub = 2;                  // centre sub-tiles per iteration
+constexpr int kBM = kTile * kQSub;        // query rows per workgroup (64)
+constexpr int kBN = kTile * kCSub;        // centres per iteration (64)
+constexpr int kThreads = 256;             // 4 waves of 64
+
+inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// One launch of sum_j k(q_i, c_j) W_j over a centre range, for every query
+// row q_i, written as partial sums per centre split.
+struct KmvArgs {
+    const float* Q;        // queries, nq x d, leading dimension ldq
+    int64_t ldq;
+    const float* qn;       // |q_i|^2, nq entries
+    const int64_t* qid;    // global row id of each query (NULL: none)
+    int64_t nq;
+    const float* C;        // centres, nc x d, leading dimension ldc
+    int64_t ldc;
+    const float* cn;       // |c_j|^2, nc entries
+    const int64_t* cid;    // global row id of each centre (NULL: j itself)
+    int64_t nc;
+    int64_t d;
+    const float* W;        // weights, >= round_up(nc, kBN) rows x ldw,
+    int64_t ldw;           //   rows >= nc and columns >= l are zero
+    int lt;                // label tiles = ldw / 32
+    float* out;            // partials [slices][out_rows][ldw]
+    int64_t out_rows;      // >= round_up(nq, kBM)
+    int64_t cps;           // centres per split, multiple of kBN
+    int splits;
+    int wl, wj;            // contraction layout: label groups x centre groups
+    int kind;              // EP_GAUSSIAN / EP_LAPLACIAN
+    float scale;           // exp2 argument scale (see kmv.hip)
+};
+
+// Chooses splits / wave layout and launches; returns the number of partial
+// slices written (splits * wj). Buffer sizes are the caller's duty; the
+// required slice count for an (nq, nc, ldw) problem comes from kmv_plan.
+struct KmvPlan {
+    int splits;
+    int wl, wj;
+    int ltw;               // label tiles per wave (compile-time variant)
+    int64_t cps;
+    int slices() const { return splits * wj; }
+};
+KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices);
+// Launches one fused pass per block of up to 1024 label columns.
+hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s);
+
+float kernel_scale(int kind, float bandwidth);
+
+// Auxiliary kernels (kernels.hip).
+hipError_t launch_row_norms(const float* X, int64_t rows, int64_t d, int64_t ld,
+                            float* out, hipStream_t s);
+hipError_t launch_gather_rows(const float* X, int64_t n, int64_t d, const float* norms,
+                              const int64_t* idx, int64_t m, int64_t m_pad,
+                              float* out, float* out_norms, int* err, hipStream_t s);
+hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pad,
+                                  int64_t ldw, int64_t m, int64_t l, const float* y,
+                                  float* f_out, float* R, float* alpha, int64_t n,
+                                  const int64_t* t, float coef, hipStream_t s);
+hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad,
+                              int64_t ldw, int64_t rows, int64_t cols, float* out,
+                              int64_t ldo, hipStream_t s);
+hipError_t launch_vt_g(const float* V, int64_t ldv, const float* G, int64_t ldg,
+                       int64_t s_rows, int64_t k, int64_t cols_pad, float* part,
+                       int slices, hipStream_t st);
+hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
+                               const float* Dk, float* W1, hipStream_t st);
+hipError_t launch_lowrank_update(const float* V, int64_t ldv, const float* W1, int64_t ldw1,
+                                 int64_t s_rows, int64_t k, int64_t l, const int64_t* r,
+                                 float* alpha, int64_t lda, float coef, hipStream_t st);
+hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d,
+                                       int kind, double bandwidth, double* Ks,
+                                       hipStream_t st);
+hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t s, int64_t k,
+                                  const double* sigma_desc_dev, float* V, int64_t ldv,
+                                  double* kp_diag, hipStream_t st);
+hipError_t launch_fill_f32(float* p, int64_t count, float v, hipStream_t st);
+
+}  // namespace ep

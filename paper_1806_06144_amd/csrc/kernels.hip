@@ -1,0 +1,364 @@
+// Auxiliary kernels of the EigenPro 2.0 step on gfx950: row norms, batch
+// gather, the deterministic split reduction fused with the residual and the
+// batch-block update (Algorithm 1 step 3), the rank-k correction applied to
+// the fixed block (Algorithm 1 step 5, Eq. 8), and the float64 subsample
+// kernel matrix of the initialisation.
+#include "ep_internal.h"
+
+#include <math.h>
+
+namespace ep {
+
+namespace {
+
+constexpr int kGT = 64;     // SIMT GEMM tile edge
+constexpr int kGK = 16;     // SIMT GEMM depth per stage
+
+__global__ void __launch_bounds__(256) row_norms_kernel(const float* X, int64_t rows,
+                                                        int64_t d, int64_t ld, float* out) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const float* x = X + row * ld;
+    double acc = 0.0;
+    for (int64_t j = lane; j < d; j += 64) {
+        const double v = x[j];
+        acc += v * v;
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_down(acc, off, 64);
+    if (lane == 0) out[row] = (float)acc;
+}
+
+__global__ void __launch_bounds__(256) gather_rows_kernel(const float* X, int64_t n, int64_t d,
+                                                          const float* norms, const int64_t* idx,
+                                                          int64_t m, float* out,
+                                                          float* out_norms, int* err) {
+    const int64_t b = blockIdx.x;
+    float* o = out + b * d;
+    int64_t src = -1;
+    if (b < m) {
+        src = idx[b];
+        if (src < 0 || src >= n) {
+            if (threadIdx.x == 0) atomicOr(err, 1);
+            src = -1;
+        }
+    }
+    if (src < 0) {
+        for (int64_t j = threadIdx.x; j < d; j += blockDim.x) o[j] = 0.f;
+        if (threadIdx.x == 0) out_norms[b] = 0.f;
+        return;
+    }
+    const float* x = X + src * d;
+    for (int64_t j = threadIdx.x; j < d; j += blockDim.x) o[j] = x[j];
+    if (threadIdx.x == 0) out_norms[b] = norms[src];
+}
+
+// F = sum of partial slices; R = F - y_b; alpha[t] -= coef * R (step 3).
+// Rows >= m and columns >= l of R are written as zero.
+__global__ void __launch_bounds__(256) reduce_residual_kernel(
+    const float* part, int slices, int64_t rows_pad, int64_t ldw, int64_t m, int64_t l,
+    const float* y, float* f_out, float* R, float* alpha, int64_t n, const int64_t* t,
+    float coef) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= rows_pad * ldw) return;
+    const int64_t b = e / ldw;
+    const int64_t c = e - b * ldw;
+    if (b >= m || c >= l) {
+        R[e] = 0.f;
+        return;
+    }
+    float f = 0.f;
+    for (int sl = 0; sl < slices; ++sl) f += part[((int64_t)sl * rows_pad + b) * ldw + c];
+    const float r = f - y[b * l + c];
+    if (f_out) f_out[b * l + c] = f;
+    R[e] = r;
+    const int64_t row = t[b];
+    if (row >= 0 && row < n) alpha[row * ldw + c] -= coef * r;
+}
+
+__global__ void __launch_bounds__(256) reduce_rows_kernel(const float* part, int slices,
+                                                          int64_t rows_pad, int64_t ldw,
+                                                          int64_t rows, int64_t cols,
+                                                          float* out, int64_t ldo) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= rows * cols) return;
+    const int64_t b = e / cols;
+    const int64_t c = e - b * cols;
+    float f = 0.f;
+    for (int sl = 0; sl < slices; ++sl) f += part[((int64_t)sl * rows_pad + b) * ldw + c];
+    out[b * ldo + c] = f;
+}
+
+// C(i, j) = sum_kk A(i, kk) B(kk, j) over kk in this block's depth range,
+// A(i, kk) = TA ? A[kk * lda + i] : A[i * lda + kk], B row-major.
+//   EPI 0: store into slice blockIdx.z of C (rows padded to a multiple of 64)
+//   EPI 1: alpha[r[i], j] += coef * C(i, j) for j < nvalid
+struct GemmArgs {
+    int64_t M, N, K, kper;
+    const float* A;
+    int64_t lda;
+    const float* B;
+    int64_t ldb;
+    float* C;
+    int64_t ldc, c_slice;
+    const int64_t* r;
+    float* alpha;
+    int64_t ld_alpha, nvalid;
+    float coef;
+};
+
+template <bool TA, int EPI>
+__global__ void __launch_bounds__(256) gemm_simt_kernel(GemmArgs g) {
+    __shared__ float As[kGK][kGT + 4];
+    __shared__ float Bs[kGK][kGT + 4];
+    const int tid = threadIdx.x;
+    const int tx = tid & 15, ty = tid >> 4;
+    const int64_t i0 = (int64_t)blockIdx.y * kGT;
+    const int64_t j0 = (int64_t)blockIdx.x * kGT;
+    const int64_t kb = (int64_t)blockIdx.z * g.kper;
+    const int64_t ke = min(g.K, kb + g.kper);
+    float acc[4][4] = {};
+    for (int64_t k0 = kb; k0 < ke; k0 += kGK) {
+        for (int e = tid; e < kGK * kGT; e += 256) {
+            const int kk = e / kGT, ii = e % kGT;
+            const int64_t gi = i0 + ii, gk = k0 + kk;
+            float v = 0.f;
+            if (gi < g.M && gk < ke) v = TA ? g.A[gk * g.lda + gi] : g.A[gi * g.lda + gk];
+            As[kk][ii] = v;
+            const int64_t gj = j0 + ii;
+            float w = 0.f;
+            if (gj < g.N && gk < ke) w = g.B[gk * g.ldb + gj];
+            Bs[kk][ii] = w;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kGK; ++kk) {
+            float a[4], b[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                a[q] = As[kk][ty * 4 + q];
+                b[q] = Bs[kk][tx * 4 + q];
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) acc[p][q] = fmaf(a[p], b[q], acc[p][q]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const int64_t gi = i0 + ty * 4 + p;
+        if (gi >= g.M) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t gj = j0 + tx * 4 + q;
+            if (EPI == 0) {
+                if (gj < g.N) g.C[blockIdx.z * g.c_slice + gi * g.ldc + gj] = acc[p][q];
+            } else {
+                if (gj < g.nvalid) g.alpha[g.r[gi] * g.ld_alpha + gj] += g.coef * acc[p][q];
+            }
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) reduce_scale_kernel(const float* part, int slices,
+                                                           int64_t k, int64_t k_pad,
+                                                           int64_t cols, const float* Dk,
+                                                           float* W1) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= k * cols) return;
+    const int64_t i = e / cols;
+    float f = 0.f;
+    for (int sl = 0; sl < slices; ++sl) f += part[(int64_t)sl * k_pad * cols + e];
+    W1[e] = Dk[i] * f;
+}
+
+// K_s[i, j] = k(x_ri, x_rj) in float64 from direct coordinate differences.
+__global__ void __launch_bounds__(256) subsample_kernel_f64(const float* Xs, int64_t s,
+                                                            int64_t d, int kind, double bw,
+                                                            double* Ks) {
+    __shared__ double Ai[kGK][kGT + 1];
+    __shared__ double Bj[kGK][kGT + 1];
+    const int tid = threadIdx.x;
+    const int tx = tid & 15, ty = tid >> 4;
+    const int64_t i0 = (int64_t)blockIdx.y * kGT;
+    const int64_t j0 = (int64_t)blockIdx.x * kGT;
+    double acc[4][4] = {};
+    for (int64_t k0 = 0; k0 < d; k0 += kGK) {
+        for (int e = tid; e < kGK * kGT; e += 256) {
+            const int ii = e / kGK, kk = e % kGK;
+            const int64_t gk = k0 + kk;
+            const int64_t gi = i0 + ii, gj = j0 + ii;
+            Ai[kk][ii] = (gi < s && gk < d) ? (double)Xs[gi * d + gk] : 0.0;
+            Bj[kk][ii] = (gj < s && gk < d) ? (double)Xs[gj * d + gk] : 0.0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kGK; ++kk) {
+            double a[4], b[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                a[q] = Ai[kk][ty * 4 + q];
+                b[q] = Bj[kk][tx * 4 + q];
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const double df = a[p] - b[q];
+                    acc[p][q] = fma(df, df, acc[p][q]);
+                }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const int64_t gi = i0 + ty * 4 + p;
+        if (gi >= s) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t gj = j0 + tx * 4 + q;
+            if (gj >= s) continue;
+            const double d2 = acc[p][q];
+            Ks[gi * s + gj] = kind == 0 ? exp(-d2 / (2.0 * bw * bw)) : exp(-sqrt(d2) / bw);
+        }
+    }
+}
+
+// V[i, j] = Z[i, k - j] (top-k eigenvectors in descending order, float32) and
+// kp_diag[i] = 1 - sum_{j<k} (sigma_j - sigma_k) Z[i, k-j]^2: the adapted
+// kernel k_G(x_ri, x_ri) at each subsample point.
+__global__ void __launch_bounds__(256) extract_eigvecs_kernel(const double* Z, int64_t ldz,
+                                                              int64_t s, int64_t k,
+                                                              const double* sig, float* V,
+                                                              int64_t ldv, double* kp_diag) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= s) return;
+    double acc = 0.0;
+    for (int64_t j = 0; j < k; ++j) {
+        const double z = Z[i + (k - j) * ldz];
+        V[i * ldv + j] = (float)z;
+        acc += (sig[j] - sig[k]) * z * z;
+    }
+    for (int64_t j = k; j < ldv; ++j) V[i * ldv + j] = 0.f;
+    kp_diag[i] = 1.0 - acc;
+}
+
+__global__ void __launch_bounds__(256) fill_kernel(float* p, int64_t count, float v) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < count) p[e] = v;
+}
+
+inline unsigned blocks_for(int64_t count, int per = 256) {
+    return (unsigned)((count + per - 1) / per);
+}
+
+}  // namespace
+
+hipError_t launch_row_norms(const float* X, int64_t rows, int64_t d, int64_t ld, float* out,
+                            hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(row_norms_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s, X, rows,
+                       d, ld, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const float* X, int64_t n, int64_t d, const float* norms,
+                              const int64_t* idx, int64_t m, int64_t m_pad, float* out,
+                              float* out_norms, int* err, hipStream_t s) {
+    if (m_pad <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)m_pad), dim3(256), 0, s, X, n, d,
+                       norms, idx, m, out, out_norms, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pad, int64_t ldw,
+                                  int64_t m, int64_t l, const float* y, float* f_out, float* R,
+                                  float* alpha, int64_t n, const int64_t* t, float coef,
+                                  hipStream_t s) {
+    hipLaunchKernelGGL(reduce_residual_kernel, dim3(blocks_for(rows_pad * ldw)), dim3(256), 0, s,
+                       part, slices, rows_pad, ldw, m, l, y, f_out, R, alpha, n, t, coef);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad, int64_t ldw,
+                              int64_t rows, int64_t cols, float* out, int64_t ldo,
+                              hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(reduce_rows_kernel, dim3(blocks_for(rows * cols)), dim3(256), 0, s, part,
+                       slices, rows_pad, ldw, rows, cols, out, ldo);
+    return hipGetLastError();
+}
+
+hipError_t launch_vt_g(const float* V, int64_t ldv, const float* G, int64_t ldg, int64_t s_rows,
+                       int64_t k, int64_t cols_pad, float* part, int slices, hipStream_t st) {
+    GemmArgs g{};
+    g.M = k;
+    g.N = cols_pad;
+    g.K = s_rows;
+    g.kper = round_up(ceil_div(s_rows, slices), kGK);
+    g.A = V;
+    g.lda = ldv;
+    g.B = G;
+    g.ldb = ldg;
+    g.C = part;
+    g.ldc = cols_pad;
+    g.c_slice = round_up(k, kGT) * cols_pad;
+    dim3 grid((unsigned)ceil_div(cols_pad, kGT), (unsigned)ceil_div(k, kGT), (unsigned)slices);
+    hipLaunchKernelGGL((gemm_simt_kernel<true, 0>), grid, dim3(256), 0, st, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
+                               const float* Dk, float* W1, hipStream_t st) {
+    hipLaunchKernelGGL(reduce_scale_kernel, dim3(blocks_for(k * cols_pad)), dim3(256), 0, st,
+                       part, slices, k, round_up(k, kGT), cols_pad, Dk, W1);
+    return hipGetLastError();
+}
+
+hipError_t launch_lowrank_update(const float* V, int64_t ldv, const float* W1, int64_t ldw1,
+                                 int64_t s_rows, int64_t k, int64_t l, const int64_t* r,
+                                 float* alpha, int64_t lda, float coef, hipStream_t st) {
+    GemmArgs g{};
+    g.M = s_rows;
+    g.N = l;
+    g.K = k;
+    g.kper = round_up(k, kGK);
+    g.A = V;
+    g.lda = ldv;
+    g.B = W1;
+    g.ldb = ldw1;
+    g.r = r;
+    g.alpha = alpha;
+    g.ld_alpha = lda;
+    g.nvalid = l;
+    g.coef = coef;
+    dim3 grid((unsigned)ceil_div(l, kGT), (unsigned)ceil_div(s_rows, kGT), 1);
+    hipLaunchKernelGGL((gemm_simt_kernel<false, 1>), grid, dim3(256), 0, st, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d, int kind,
+                                       double bandwidth, double* Ks, hipStream_t st) {
+    dim3 grid((unsigned)ceil_div(s, kGT), (unsigned)ceil_div(s, kGT));
+    hipLaunchKernelGGL(subsample_kernel_f64, grid, dim3(256), 0, st, Xs, s, d, kind, bandwidth,
+                       Ks);
+    return hipGetLastError();
+}
+
+hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t s, int64_t k,
+                                  const double* sigma_desc_dev, float* V, int64_t ldv,
+                                  double* kp_diag, hipStream_t st) {
+    hipLaunchKernelGGL(extract_eigvecs_kernel, dim3(blocks_for(s)), dim3(256), 0, st, Z, ldz, s,
+                       k, sigma_desc_dev, V, ldv, kp_diag);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, int64_t count, float v, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(count)), dim3(256), 0, st, p, count, v);
+    return hipGetLastError();
+}
+
+}  // namespace ep

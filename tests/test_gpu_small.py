@@ -1,0 +1,123 @@
+"""GPU vs fp64 oracle on small seeded problems that exercise the edges of
+the tiling: ragged query / centre / feature / label tails, label blocks
+above 1024, k = 0 (plain SGD), s = n, a single-point batch, a full batch,
+batch rows that are also subsample rows, and both kernels."""
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_common import Gpu, TOL_STEP, TOL_EPOCH, kernel_id, lowrank, rel
+
+CASES = [
+    # kernel, n, d, l, s, k, m, bw
+    ("gaussian", 300, 17, 3, 50, 5, 40, 1.0),
+    ("laplacian", 1000, 64, 33, 200, 20, 130, 1.5),
+    ("gaussian", 777, 36, 10, 777, 30, 777, 0.9),
+    ("gaussian", 129, 8, 1, 20, 0, 1, 1.0),
+    ("laplacian", 2000, 100, 160, 300, 40, 257, 2.0),
+    ("gaussian", 600, 40, 1100, 64, 10, 70, 1.2),
+    ("laplacian", 5000, 130, 7, 400, 60, 700, 3.0),
+]
+
+
+def _problem(n, d, l, seed):
+    rng = np.random.default_rng(seed)
+    X = (rng.standard_normal((n, d)) / np.sqrt(d)).astype(np.float32)
+    Y = np.eye(l, dtype=np.float32)[rng.integers(0, l, n)]
+    a0 = (rng.standard_normal((n, l)) / np.sqrt(n)).astype(np.float32)
+    return X, Y, a0, rng
+
+
+def _batch(rng, n, r, m):
+    """m distinct indices; about a quarter of them also subsample rows."""
+    q = min(max(1, m // 4), len(r), m)
+    head = r[:q]
+    rest = rng.choice(np.setdiff1d(np.arange(n), head), m - q, replace=False)
+    t = np.concatenate([head, rest]).astype(np.int64)
+    rng.shuffle(t)
+    return t
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", CASES, ids=[f"{c[0][:3]}-n{c[1]}-d{c[2]}-l{c[3]}-s{c[4]}-k{c[5]}-m{c[6]}" for c in CASES])
+def test_one_step_setup_predict(case):
+    kernel, n, d, l, s, k, m, bw = case
+    X, Y, a0, rng = _problem(n, d, l, 1)
+    r = rng.choice(n, s, replace=False)
+    t = _batch(rng, n, r, m)
+    Z = (rng.standard_normal((77, d)) / np.sqrt(d)).astype(np.float32)
+    st = oracle.setup(X, kernel_id(kernel), bw, s, k, r)
+    a1_o, F_o = oracle.step(st, a0, t, Y[t])
+    P_o = oracle.predict(X, a1_o, Z, kernel_id(kernel), bw)
+    with Gpu(X, l, kernel, bw, s, k, r) as g:
+        info = g.info
+        assert info.m == st.m
+        assert info.m_star == pytest.approx(st.m_star, rel=1e-9)
+        assert info.beta == pytest.approx(st.beta, rel=1e-9, abs=1e-12)
+        assert info.sigma_k1 == pytest.approx(st.sigma[k], rel=1e-9)
+        sigma, D, V, r_back = g.preconditioner()
+        np.testing.assert_array_equal(r_back, r)
+        np.testing.assert_allclose(sigma, st.sigma, rtol=1e-9)
+        if k:
+            assert rel(lowrank(V, D), lowrank(st.V, st.D)) < 1e-5
+        g.set_alpha(a0)
+        F = g.step(t, Y[t])
+        a1 = g.alpha()
+        P = g.predict(Z)
+    assert rel(F, F_o) < TOL_STEP
+    assert rel(a1 - a0, a1_o - a0) < TOL_STEP
+    assert rel(P, P_o) < TOL_STEP
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("kernel,k", [("gaussian", 12), ("laplacian", 0)])
+def test_epochs_from_zero(kernel, k):
+    n, d, l, s = 1500, 32, 4, 250
+    X, Y, _, rng = _problem(n, d, l, 2)
+    r = rng.choice(n, s, replace=False)
+    st = oracle.setup(X, kernel_id(kernel), 1.0, s, k, r)
+    m = min(st.m, 300)
+    a = np.zeros((n, l))
+    with Gpu(X, l, kernel, 1.0, s, k, r) as g:
+        for e in range(2):
+            p = rng.permutation(n)
+            batches = [p[i:i + m] for i in range(0, n, m)]
+            for t in batches:
+                a, _ = oracle.step(st, a, t, Y[t])
+                g.step(t, Y[t], want_f=False)
+        a_gpu = g.alpha()
+    assert rel(a_gpu, a) < TOL_EPOCH
+
+
+@pytest.mark.gpu
+def test_error_paths_and_alpha_roundtrip():
+    import torch
+    import paper_1806_06144_amd as ep
+    n, d, l = 200, 12, 3
+    X, Y, a0, rng = _problem(n, d, l, 3)
+    with pytest.raises(ep.EigenProError) as ei:
+        Gpu(X, l, "gaussian", 1.0, 20, 4, np.array([1] * 20))
+    assert ei.value.code == ep.EP_EINVAL
+    with Gpu(X, l, "gaussian", 1.0, 20, 4, None, seed=7) as g:
+        _, _, _, r = g.preconditioner()
+        assert len(np.unique(r)) == 20 and r.min() >= 0 and r.max() < n
+        g.set_alpha(a0)
+        np.testing.assert_array_equal(g.alpha(), a0)
+        # an index outside [0, n) is neither read nor written; ep_sync reports it
+        bad = np.array([3, n + 5, 7], dtype=np.int64)
+        g.step(bad, Y[:3], want_f=False)
+        with pytest.raises(ep.EigenProError) as ei:
+            ep.ep_sync(g.ctx)
+        assert ei.value.code == ep.EP_EINDEX
+        ep.ep_sync(g.ctx)              # flag is cleared once reported
+        # repeated indices are rejected when checks are on
+        ep.ep_set_checks(g.ctx, True)
+        with pytest.raises(ep.EigenProError) as ei:
+            g.step(np.array([4, 9, 4]), Y[:3], want_f=False)
+        assert ei.value.code == ep.EP_EINDEX
+        with pytest.raises(ep.EigenProError) as ei:
+            ep.ep_step(g.ctx, g.t(np.array([1], dtype=np.int64)), 0, g.t(Y[:1]))
+        assert ei.value.code == ep.EP_EINVAL
+        # empty prediction is a no-op
+        ep.ep_predict(g.ctx, g.t(X[:1]), 0, torch.empty((1, l), device="cuda:0"))
