@@ -49,6 +49,10 @@ def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                           "or python -m paper_1806_06144_amd.build")
+    # torch ships its own HIP runtime under the same soname; loading torch
+    # first makes the library bind to that one, so the process holds a
+    # single runtime (two copies would not see each other's devices).
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
     sig = {

@@ -53,12 +53,15 @@ def test_one_step_setup_predict(case):
     with Gpu(X, l, kernel, bw, s, k, r) as g:
         info = g.info
         assert info.m == st.m
-        assert info.m_star == pytest.approx(st.m_star, rel=1e-9)
-        assert info.beta == pytest.approx(st.beta, rel=1e-9, abs=1e-12)
-        assert info.sigma_k1 == pytest.approx(st.sigma[k], rel=1e-9)
+        # setup is float64 on both sides; the oracle's distance expansion
+        # leaves up to ~1e-8 on the Laplacian diagonal (square root of
+        # rounding noise), so setup scalars are compared at 1e-6
+        assert info.m_star == pytest.approx(st.m_star, rel=1e-6)
+        assert info.beta == pytest.approx(st.beta, rel=1e-6, abs=1e-9)
+        assert info.sigma_k1 == pytest.approx(st.sigma[k], rel=1e-6)
         sigma, D, V, r_back = g.preconditioner()
         np.testing.assert_array_equal(r_back, r)
-        np.testing.assert_allclose(sigma, st.sigma, rtol=1e-9)
+        np.testing.assert_allclose(sigma, st.sigma, rtol=1e-6)
         if k:
             assert rel(lowrank(V, D), lowrank(st.V, st.D)) < 1e-5
         g.set_alpha(a0)
