@@ -1,0 +1,218 @@
+"""Throughput of one EigenPro 2.0 iteration on one MI355X.
+
+A step is one call of ep_step: gather the batch, the fused kernel-block
+contraction F = K(X_t, X) alpha, residual and batch-block update, the
+subsample correction K(X_r, X_t) R through the same fused kernel, and the
+rank-k update of the fixed block (Algorithm 1 steps 1-5).
+
+Default workload: the ImageNet-feature-shaped synthetic problem (n = 1.28M
+centres, d = 2048, l = 1000 one-hot labels, Gaussian bandwidth 20, s = 20000,
+k = 200, batch = the analytic m*). Inputs are generated on the host, uploaded
+once, and are resident in HBM before timing starts.
+
+Prints one JSON line. ``value`` is kernel entries per second (m * n per
+step over the wall time of the timed steps).
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3     # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kmv_source_sha():
+    with open(os.path.join(ROOT, "paper_1806_06144_amd", "csrc", "kmv.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the fused kernel from committed rocprofv3
+    counter runs, if they were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "kmv_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = rec.get(workload)
+    if not entry or entry.get("kmv_source_sha") != kmv_source_sha():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(X, alpha_host, cfg, target_s=15.0):
+    """The fp64 oracle's kernel-block contraction F = K(X_t, X) alpha (the
+    dominant part of a step) on a bounded sample of batch rows against all n
+    centres, scaled to kernel entries per second."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    rng = np.random.default_rng(123)
+    kid = {"gaussian": oracle.GAUSSIAN, "laplacian": oracle.LAPLACIAN}[cfg.kernel]
+    rows = 8
+    t0 = time.perf_counter()
+    oracle.predict(X, alpha_host, X[rng.choice(X.shape[0], rows, replace=False)], kid,
+                   cfg.bandwidth)
+    dt = time.perf_counter() - t0
+    rows2 = int(max(rows, min(X.shape[0], 20000, rows * target_s / max(dt, 1e-3))))
+    if rows2 > rows * 1.5:
+        t0 = time.perf_counter()
+        oracle.predict(X, alpha_host, X[rng.choice(X.shape[0], rows2, replace=False)], kid,
+                       cfg.bandwidth)
+        dt = time.perf_counter() - t0
+        rows = rows2
+    return {
+        "value": rows * X.shape[0] / dt,
+        "unit": "entries/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"fp64 oracle F = K(X_t, X) alpha for {rows} batch rows against all "
+                   f"{X.shape[0]} centres (d={X.shape[1]}, l={alpha_host.shape[1]}), "
+                   f"{dt:.1f} s"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="imagenet")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--s", type=int, default=None,
+                    help="override the subsample size (experiments only)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "this build has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_1806_06144_amd as ep
+
+    cfg = synth.get_config(args.config)
+    if args.s is not None:
+        cfg = synth.get_config(args.config, s=args.s)
+    dev = torch.device("cuda:0")
+    log(f"workload {cfg.name}: n={cfg.n} d={cfg.d} l={cfg.l} s={cfg.s} k={cfg.k}")
+    t0 = time.perf_counter()
+    X = synth.features(cfg, 0)
+    labels = synth.class_labels(cfg, X, 0)
+    r = synth.subsample_indices(cfg, 0)
+    log(f"generated inputs in {time.perf_counter() - t0:.1f} s")
+    Xd = torch.from_numpy(X).to(dev)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
+                            sub_idx=r, stream=stream)
+    m = int(cfg.m) if cfg.m else int(info.m)
+    log(f"setup {info.setup_ms / 1e3:.1f} s: m*={info.m_star:.1f} m={m} beta={info.beta:.4f} "
+        f"sigma_k+1={info.sigma_k1:.4f} eta={info.eta:.1f}")
+
+    nb = args.warmup + args.steps
+    perm = synth.epoch_permutation(cfg.n, 0, 0)
+    batches = [perm[i * m:(i + 1) * m] for i in range(nb)]
+    if any(len(b) != m for b in batches):
+        raise SystemExit("not enough full batches in one epoch for the requested steps")
+    t_dev = [torch.from_numpy(b).to(dev) for b in batches]
+    y_dev = [torch.from_numpy(synth.one_hot(labels[b], cfg.l)).to(dev) for b in batches]
+
+    for i in range(args.warmup):
+        ep.ep_step(ctx, t_dev[i], m, y_dev[i])
+    ep.ep_sync(ctx)
+    ep.ep_timing_enable(ctx, True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.warmup, nb):
+        ep.ep_step(ctx, t_dev[i], m, y_dev[i])
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    ep.ep_sync(ctx)
+    tim = ep.ep_timing_read(ctx)
+    ep.ep_timing_enable(ctx, False)
+
+    sec_per_step = (t_end - t_start) / args.steps
+    n, d, l, s, k = cfg.n, cfg.d, cfg.l, cfg.s, cfg.k
+    entries = m * n
+    kmv_flops = 2.0 * m * n * (d + l)
+    step_flops = 2.0 * m * (n + s) * (d + l) + 4.0 * s * k * l
+    kmv_avg_s = tim.kmv_ms / 1e3 / max(tim.kmv_launches, 1)
+    achieved = kmv_flops / kmv_avg_s / 1e12
+    workload = f"{cfg.name}-shaped n={n} d={d} l={l} {cfg.kernel} bw={cfg.bandwidth:g} s={s} k={k} m={m}"
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("calibration copy: 3 x 1 GiB device-to-device")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        alpha = torch.empty((n, l), dtype=torch.float32, device=dev)
+        ep.ep_get_alpha(ctx, alpha)
+        ep.ep_sync(ctx)
+        log("timing the oracle on a bounded sample")
+        cpu = cpu_baseline(X, alpha.cpu().numpy(), cfg)
+    ep.ep_destroy(ctx)
+
+    traffic = measured_traffic(workload)
+    out = {
+        "metric": "kernel entries/s (m*n per step)",
+        "value": entries / sec_per_step,
+        "unit": "entries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sec_per_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": workload, "n": n, "d": d, "l": l, "s": s, "k": k, "m": m,
+                   "kernel": cfg.kernel, "bandwidth": cfg.bandwidth},
+        "tflops_fused_kernel": achieved,
+        "tflops_whole_step": step_flops / sec_per_step / 1e12,
+        "s_per_epoch_est": (n / m) * sec_per_step,
+        "setup_s": info.setup_ms / 1e3,
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_FP32_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+            "traffic": traffic,
+            "kernel": "kmv_kernel (fused distance -> kernel -> contraction, step 2)",
+            "avg_launch_ms": kmv_avg_s * 1e3,
+            "launches": int(tim.kmv_launches),
+            "flops_per_launch": kmv_flops,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -244,48 +244,46 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
                                c->s_pad, c->Xs.as<float>(), c->xs_norms.as<float>(),
                                c->err.as<int>(), st));
 
-    // K_s in float64 and its top k+1 eigenpairs (Algorithm 1 initialisation)
-    DevBuf Ks, Z, W, kp, sig_dev, iinfo;
+    // K_s in float64 and its top k+1 eigenpairs (Algorithm 1 initialisation).
+    // The full divide-and-conquer eigensolver is used: on this device it is
+    // much faster than the subset solvers, and K_s is small next to X.
+    DevBuf Ks, W, E, kp, sig_dev, iinfo;
     struct Free {
-        DevBuf* b[5];
+        DevBuf* b[6];
         ~Free() {
             for (DevBuf* x : b) x->release();
         }
-    } guard{{&Ks, &Z, &W, &kp, &sig_dev}};
+    } guard{{&Ks, &W, &E, &kp, &sig_dev, &iinfo}};
     HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
-    HIP_TRY(Z.ensure((size_t)s * s * sizeof(double)));
     HIP_TRY(W.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(E.ensure((size_t)s * sizeof(double)));
     HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
     HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
-    HIP_TRY(iinfo.ensure(2 * sizeof(rocblas_int)));
+    HIP_TRY(iinfo.ensure(sizeof(rocblas_int)));
     HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
                                         Ks.as<double>(), st));
 
     rocblas_handle h = nullptr;
-    if (rocblas_create_handle(&h) != rocblas_status_success) {
-        iinfo.release();
+    if (rocblas_create_handle(&h) != rocblas_status_success)
         return fail(EP_EDEVICE, "rocblas_create_handle failed");
-    }
     rocblas_set_stream(h, st);
     rocblas_int* dinfo = iinfo.as<rocblas_int>();
-    const rocblas_status rs = rocsolver_dsyevdx(
-        h, rocblas_evect_original, rocblas_erange_index, rocblas_fill_upper, (rocblas_int)s,
-        Ks.as<double>(), (rocblas_int)s, 0.0, 0.0, (rocblas_int)(s - k), (rocblas_int)s, dinfo,
-        W.as<double>(), Z.as<double>(), (rocblas_int)s, dinfo + 1);
+    // eigenvalues ascending in W, eigenvectors overwrite K_s (column-major)
+    const rocblas_status rs =
+        rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)s,
+                         Ks.as<double>(), (rocblas_int)s, W.as<double>(), E.as<double>(), dinfo);
     rocblas_destroy_handle(h);
-    if (rs != rocblas_status_success) {
-        iinfo.release();
-        return fail(EP_EDEVICE, "rocsolver_dsyevdx returned status %d", (int)rs);
-    }
-    rocblas_int hinfo[2] = {0, 0};
+    if (rs != rocblas_status_success)
+        return fail(EP_EDEVICE, "rocsolver_dsyevd returned status %d", (int)rs);
+    rocblas_int hinfo = 0;
     std::vector<double> w_asc(k + 1);
-    HIP_TRY(hipMemcpyAsync(hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.p, (k + 1) * sizeof(double), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(&hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.as<double>() + (s - k - 1), (k + 1) * sizeof(double),
+                           hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
-    iinfo.release();
-    if (hinfo[1] != 0 || hinfo[0] != (rocblas_int)(k + 1))
-        return fail(EP_ENUMERIC, "eigensolve failed: info=%d, found %d of %lld eigenpairs",
-                    (int)hinfo[1], (int)hinfo[0], (long long)(k + 1));
+    if (hinfo != 0) return fail(EP_ENUMERIC, "eigensolve failed: info=%d", (int)hinfo);
+    // top k+1 eigenvectors: the last k+1 columns
+    const double* Z = Ks.as<double>() + (size_t)(s - k - 1) * s;
     c->sigma.assign(w_asc.rbegin(), w_asc.rend());
     if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
         return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
@@ -300,7 +298,7 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
     HIP_TRY(hipMemcpyAsync(c->Dk.p, dk.data(), c->k_ld * sizeof(float), hipMemcpyHostToDevice, st));
     HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
                            hipMemcpyHostToDevice, st));
-    HIP_TRY(launch_extract_eigvecs(Z.as<double>(), s, s, k, sig_dev.as<double>(), c->V.as<float>(),
+    HIP_TRY(launch_extract_eigvecs(Z, s, s, k, sig_dev.as<double>(), c->V.as<float>(),
                                    c->k_ld, kp.as<double>(), st));
     std::vector<double> kpd(s);
     HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
