@@ -98,6 +98,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--s", type=int, default=None,
                     help="override the subsample size (experiments only)")
+    ap.add_argument("--save-setup", default=None,
+                    help="write the subsample and eigensystem to this .npz")
+    ap.add_argument("--load-setup", default=None,
+                    help="rebuild the context from a saved setup (ep_restore; no eigensolve)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -123,8 +127,16 @@ def main():
     Xd = torch.from_numpy(X).to(dev)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
-                            sub_idx=r, stream=stream)
+    if args.load_setup:
+        sv = np.load(args.load_setup)
+        ctx, info = ep.ep_restore(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s,
+                                  cfg.k, sv["r"], sv["sigma"], sv["V"], stream=stream)
+    else:
+        ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s,
+                                cfg.k, sub_idx=r, stream=stream)
+    if args.save_setup:
+        sigma, _, V, r_used = ep.ep_get_preconditioner(ctx, info)
+        np.savez(args.save_setup, r=r_used, sigma=sigma, V=V)
     m = int(cfg.m) if cfg.m else int(info.m)
     log(f"setup {info.setup_ms / 1e3:.1f} s: m*={info.m_star:.1f} m={m} beta={info.beta:.4f} "
         f"sigma_k+1={info.sigma_k1:.4f} eta={info.eta:.1f}")

@@ -87,6 +87,24 @@ int ep_setup(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
              ep_info* info);
 
 /*
+ * ep_restore — rebuild a context from a saved setup (checkpoint / resume):
+ * the same as ep_setup with the subsample and eigensystem supplied instead
+ * of computed, so no eigensolver runs.
+ *   sub_idx  host, the s subsample indices that were used (required).
+ *   sigma    host double[k+1], descending eigenvalues of K_s (required).
+ *   V        host float[s*k], row-major top-k eigenvectors, row i for
+ *            sub_idx[i] (may be NULL when k = 0).
+ * beta, m* and eta are recomputed from sigma and V. alpha is set to 0; use
+ * ep_set_alpha to restore it. ep_get_preconditioner returns exactly these
+ * three arrays. Errors: as ep_setup, plus EP_EINVAL for missing arrays,
+ * non-finite or increasing sigma, sigma_{k+1} <= 0, non-finite V.
+ */
+int ep_restore(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
+               int kernel, float bandwidth, int64_t s, int64_t k,
+               const int64_t* sub_idx, const double* sigma, const float* V,
+               void* hip_stream, ep_info* info);
+
+/*
  * ep_step — one iteration of Algorithm 1 (steps 1-5) on a batch of m points.
  *
  *   t       device int64[m]: batch indices, distinct, in [0, n).

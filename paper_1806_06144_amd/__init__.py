@@ -58,6 +58,8 @@ def _load():
     sig = {
         "ep_setup": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P,
                          ctypes.c_uint64, P, ctypes.POINTER(EpInfo)]),
+        "ep_restore": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P, P, P, P,
+                           ctypes.POINTER(EpInfo)]),
         "ep_step": (I, [P, P, I64, P, P]),
         "ep_predict": (I, [P, P, I64, P]),
         "ep_get_alpha": (I, [P, P]),
@@ -149,6 +151,27 @@ def ep_setup(X, n, d, l, kernel, bandwidth, s, k, sub_idx=None, seed=0, stream=N
     info = EpInfo()
     _check(_lib.ep_setup(ctypes.byref(ctx), xp, n, d, l, kernel, bandwidth, s, k, sub_ptr,
                          seed, _stream_handle(stream), ctypes.byref(info)))
+    return ctx, info
+
+
+def ep_restore(X, n, d, l, kernel, bandwidth, s, k, sub_idx, sigma, V, stream=None):
+    """Rebuild a context from a saved setup (sub_idx, sigma[k+1], V[s, k] as
+    returned by ep_get_preconditioner). Returns (ctx, EpInfo)."""
+    import numpy as np
+    torch = _torch()
+    if isinstance(kernel, str):
+        kernel = KERNELS[kernel]
+    r = np.ascontiguousarray(np.asarray(sub_idx, dtype=np.int64))
+    sg = np.ascontiguousarray(np.asarray(sigma, dtype=np.float64))
+    if r.shape != (s,) or sg.shape != (k + 1,):
+        raise ValueError("sub_idx must hold s entries and sigma k+1")
+    Vh = np.ascontiguousarray(np.asarray(V, dtype=np.float32).reshape(s, k)) if k else None
+    ctx = ctypes.c_void_p()
+    info = EpInfo()
+    _check(_lib.ep_restore(ctypes.byref(ctx), _ptr(X, torch.float32), n, d, l, kernel,
+                           bandwidth, s, k, r.ctypes.data, sg.ctypes.data,
+                           Vh.ctypes.data if Vh is not None else None,
+                           _stream_handle(stream), ctypes.byref(info)))
     return ctx, info
 
 

@@ -192,7 +192,96 @@ struct DeviceGuard {
     }
 };
 
-int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
+// Top k+1 eigenpairs of K_s = [k(x_ri, x_rj)] (Algorithm 1 initialisation):
+// K_s is formed in float64 and solved with the full divide-and-conquer
+// eigensolver (on this device much faster than the subset solvers; K_s is
+// small next to X). Fills c->sigma, c->V and the adapted kernel's diagonal
+// k_G(x_ri, x_ri) at the subsample points.
+int eigensystem_from_solver(ep_ctx* c, std::vector<double>& kpd) {
+    const int64_t s = c->s, k = c->k, d = c->d;
+    hipStream_t st = c->stream;
+    DevBuf Ks, W, E, kp, sig_dev, iinfo;
+    struct Free {
+        DevBuf* b[6];
+        ~Free() {
+            for (DevBuf* x : b) x->release();
+        }
+    } guard{{&Ks, &W, &E, &kp, &sig_dev, &iinfo}};
+    HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
+    HIP_TRY(W.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(E.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
+    HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
+    HIP_TRY(iinfo.ensure(sizeof(rocblas_int)));
+    HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
+                                        Ks.as<double>(), st));
+
+    rocblas_handle h = nullptr;
+    if (rocblas_create_handle(&h) != rocblas_status_success)
+        return fail(EP_EDEVICE, "rocblas_create_handle failed");
+    rocblas_set_stream(h, st);
+    rocblas_int* dinfo = iinfo.as<rocblas_int>();
+    // eigenvalues ascending in W, eigenvectors overwrite K_s (column-major)
+    const rocblas_status rs =
+        rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)s,
+                         Ks.as<double>(), (rocblas_int)s, W.as<double>(), E.as<double>(), dinfo);
+    rocblas_destroy_handle(h);
+    if (rs != rocblas_status_success)
+        return fail(EP_EDEVICE, "rocsolver_dsyevd returned status %d", (int)rs);
+    rocblas_int hinfo = 0;
+    std::vector<double> w_asc(k + 1);
+    HIP_TRY(hipMemcpyAsync(&hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.as<double>() + (s - k - 1), (k + 1) * sizeof(double),
+                           hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    if (hinfo != 0) return fail(EP_ENUMERIC, "eigensolve failed: info=%d", (int)hinfo);
+    c->sigma.assign(w_asc.rbegin(), w_asc.rend());
+    if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
+        return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
+    // top k+1 eigenvectors are the last k+1 columns
+    const double* Z = Ks.as<double>() + (size_t)(s - k - 1) * s;
+    HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_extract_eigvecs(Z, s, s, k, sig_dev.as<double>(), c->V.as<float>(), c->k_ld,
+                                   kp.as<double>(), st));
+    kpd.resize(s);
+    HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return EP_OK;
+}
+
+// Eigensystem handed in by the caller (a saved setup): sigma descending,
+// V row-major s x k.
+int eigensystem_from_saved(ep_ctx* c, const double* sigma, const float* V,
+                           std::vector<double>& kpd) {
+    const int64_t s = c->s, k = c->k;
+    c->sigma.assign(sigma, sigma + k + 1);
+    for (int64_t i = 0; i <= k; ++i) {
+        if (!std::isfinite(c->sigma[i]) || (i > 0 && c->sigma[i] > c->sigma[i - 1]))
+            return fail(EP_EINVAL, "sigma must be finite and non-increasing");
+    }
+    if (!(c->sigma[k] > 0.0)) return fail(EP_EINVAL, "sigma_{k+1} must be positive");
+    if (k > 0 && !V) return fail(EP_EINVAL, "V is NULL");
+    kpd.assign(s, 1.0);
+    for (int64_t i = 0; i < s; ++i) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < k; ++j) {
+            const double v = V[i * k + j];
+            if (!std::isfinite(v)) return fail(EP_EINVAL, "V holds a non-finite value");
+            acc += (c->sigma[j] - c->sigma[k]) * v * v;
+        }
+        kpd[i] = 1.0 - acc;
+    }
+    if (k > 0)
+        HIP_TRY(hipMemcpyAsync(c->V.p, V, (size_t)s * k * sizeof(float), hipMemcpyHostToDevice,
+                               c->stream));
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    return EP_OK;
+}
+
+int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sigma_in,
+             const float* V_in) {
+    std::vector<double> kpd;
     const int64_t n = c->n, d = c->d, s = c->s, k = c->k;
     hipStream_t st = c->stream;
 
@@ -244,49 +333,9 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
                                c->s_pad, c->Xs.as<float>(), c->xs_norms.as<float>(),
                                c->err.as<int>(), st));
 
-    // K_s in float64 and its top k+1 eigenpairs (Algorithm 1 initialisation).
-    // The full divide-and-conquer eigensolver is used: on this device it is
-    // much faster than the subset solvers, and K_s is small next to X.
-    DevBuf Ks, W, E, kp, sig_dev, iinfo;
-    struct Free {
-        DevBuf* b[6];
-        ~Free() {
-            for (DevBuf* x : b) x->release();
-        }
-    } guard{{&Ks, &W, &E, &kp, &sig_dev, &iinfo}};
-    HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
-    HIP_TRY(W.ensure((size_t)s * sizeof(double)));
-    HIP_TRY(E.ensure((size_t)s * sizeof(double)));
-    HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
-    HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
-    HIP_TRY(iinfo.ensure(sizeof(rocblas_int)));
-    HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
-                                        Ks.as<double>(), st));
-
-    rocblas_handle h = nullptr;
-    if (rocblas_create_handle(&h) != rocblas_status_success)
-        return fail(EP_EDEVICE, "rocblas_create_handle failed");
-    rocblas_set_stream(h, st);
-    rocblas_int* dinfo = iinfo.as<rocblas_int>();
-    // eigenvalues ascending in W, eigenvectors overwrite K_s (column-major)
-    const rocblas_status rs =
-        rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)s,
-                         Ks.as<double>(), (rocblas_int)s, W.as<double>(), E.as<double>(), dinfo);
-    rocblas_destroy_handle(h);
-    if (rs != rocblas_status_success)
-        return fail(EP_EDEVICE, "rocsolver_dsyevd returned status %d", (int)rs);
-    rocblas_int hinfo = 0;
-    std::vector<double> w_asc(k + 1);
-    HIP_TRY(hipMemcpyAsync(&hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.as<double>() + (s - k - 1), (k + 1) * sizeof(double),
-                           hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipStreamSynchronize(st));
-    if (hinfo != 0) return fail(EP_ENUMERIC, "eigensolve failed: info=%d", (int)hinfo);
-    // top k+1 eigenvectors: the last k+1 columns
-    const double* Z = Ks.as<double>() + (size_t)(s - k - 1) * s;
-    c->sigma.assign(w_asc.rbegin(), w_asc.rend());
-    if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
-        return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
+    int rc = sigma_in ? eigensystem_from_saved(c, sigma_in, V_in, kpd)
+                      : eigensystem_from_solver(c, kpd);
+    if (rc) return rc;
 
     // D_i = (1 - sigma_{k+1}/sigma_i) / sigma_i (Section 4, Eq. 8 with q = k+1)
     c->D.resize(k);
@@ -296,12 +345,6 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed) {
         dk[i] = (float)c->D[i];
     }
     HIP_TRY(hipMemcpyAsync(c->Dk.p, dk.data(), c->k_ld * sizeof(float), hipMemcpyHostToDevice, st));
-    HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
-                           hipMemcpyHostToDevice, st));
-    HIP_TRY(launch_extract_eigvecs(Z, s, s, k, sig_dev.as<double>(), c->V.as<float>(),
-                                   c->k_ld, kp.as<double>(), st));
-    std::vector<double> kpd(s);
-    HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
     int herr = 0;
     HIP_TRY(hipMemcpyAsync(&herr, c->err.p, sizeof(int), hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
@@ -346,9 +389,13 @@ extern "C" {
 
 const char* ep_last_error(void) { return g_err.c_str(); }
 
-int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
-             float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
-             void* hip_stream, ep_info* info) {
+}  // extern "C"
+
+namespace {
+
+int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
+           float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
+           void* hip_stream, ep_info* info, const double* sigma, const float* V) {
     g_err.clear();
     if (!out) return fail(EP_EINVAL, "ctx out-pointer is NULL");
     *out = nullptr;
@@ -378,7 +425,7 @@ int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int 
     c->kind = kernel;
     c->bandwidth = bandwidth;
     c->scale = kernel_scale(kernel, bandwidth);
-    const int rc = do_setup(c, sub_idx, seed);
+    const int rc = do_setup(c, sub_idx, seed, sigma, V);
     if (rc != EP_OK) {
         (void)hipStreamSynchronize(c->stream);
         delete c;
@@ -389,6 +436,27 @@ int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int 
     if (info) *info = c->info;
     *out = c;
     return EP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
+             float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
+             void* hip_stream, ep_info* info) {
+    return create(out, X, n, d, l, kernel, bandwidth, s, k, sub_idx, seed, hip_stream, info,
+                  nullptr, nullptr);
+}
+
+int ep_restore(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
+               float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx,
+               const double* sigma, const float* V, void* hip_stream, ep_info* info) {
+    g_err.clear();
+    if (!sub_idx) return fail(EP_EINVAL, "ep_restore needs the saved sub_idx");
+    if (!sigma) return fail(EP_EINVAL, "ep_restore needs the saved sigma");
+    return create(out, X, n, d, l, kernel, bandwidth, s, k, sub_idx, 0, hip_stream, info, sigma,
+                  V);
 }
 
 int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_out) {
@@ -435,7 +503,7 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     // step 3: R = F - y_b; alpha_t -= c R
     const double coef = 1.0 / (c->info.beta + (double)(m - 1) * c->info.lambda_k1);
     HIP_TRY(launch_reduce_residual(c->part.as<float>(), slices, rows_pad, c->l_pad, m, c->l, y_b,
-                                   f_out, R, alpha, c->n, t, (float)coef, st));
+                                   f_out, R, m_pad, alpha, c->n, t, (float)coef, st));
     if (c->k > 0) {
         // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
         rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(), c->r_dev.as<int64_t>(),

@@ -9,10 +9,10 @@ namespace ep {
 // Tile geometry of the fused kernel-block contraction (kmv.hip).
 constexpr int kTile = 32;                 // MFMA 32x32 output tile edge
 constexpr int kQSub = 2;                  // query sub-tiles per workgroup
-constexpr int kCSub = 2;                  // centre sub-tiles per iteration
+constexpr int kCSub = 4;                  // centre sub-tiles per iteration
 constexpr int kBM = kTile * kQSub;        // query rows per workgroup (64)
-constexpr int kBN = kTile * kCSub;        // centres per iteration (64)
-constexpr int kThreads = 256;             // 4 waves of 64
+constexpr int kBN = kTile * kCSub;        // centres per iteration (128)
+constexpr int kThreads = 512;             // 8 waves of 64
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -65,10 +65,12 @@ hipError_t launch_row_norms(const float* X, int64_t rows, int64_t d, int64_t ld,
 hipError_t launch_gather_rows(const float* X, int64_t n, int64_t d, const float* norms,
                               const int64_t* idx, int64_t m, int64_t m_pad,
                               float* out, float* out_norms, int* err, hipStream_t s);
+// R gets r_rows rows (zero beyond m) so that it can serve as the weights of
+// a fused pass whose centres are the batch rows.
 hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pad,
                                   int64_t ldw, int64_t m, int64_t l, const float* y,
-                                  float* f_out, float* R, float* alpha, int64_t n,
-                                  const int64_t* t, float coef, hipStream_t s);
+                                  float* f_out, float* R, int64_t r_rows, float* alpha,
+                                  int64_t n, const int64_t* t, float coef, hipStream_t s);
 hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad,
                               int64_t ldw, int64_t rows, int64_t cols, float* out,
                               int64_t ldo, hipStream_t s);

@@ -57,10 +57,10 @@ __global__ void __launch_bounds__(256) gather_rows_kernel(const float* X, int64_
 // Rows >= m and columns >= l of R are written as zero.
 __global__ void __launch_bounds__(256) reduce_residual_kernel(
     const float* part, int slices, int64_t rows_pad, int64_t ldw, int64_t m, int64_t l,
-    const float* y, float* f_out, float* R, float* alpha, int64_t n, const int64_t* t,
-    float coef) {
+    const float* y, float* f_out, float* R, int64_t r_rows, float* alpha, int64_t n,
+    const int64_t* t, float coef) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= rows_pad * ldw) return;
+    if (e >= r_rows * ldw) return;
     const int64_t b = e / ldw;
     const int64_t c = e - b * ldw;
     if (b >= m || c >= l) {
@@ -275,10 +275,10 @@ hipError_t launch_gather_rows(const float* X, int64_t n, int64_t d, const float*
 
 hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pad, int64_t ldw,
                                   int64_t m, int64_t l, const float* y, float* f_out, float* R,
-                                  float* alpha, int64_t n, const int64_t* t, float coef,
-                                  hipStream_t s) {
-    hipLaunchKernelGGL(reduce_residual_kernel, dim3(blocks_for(rows_pad * ldw)), dim3(256), 0, s,
-                       part, slices, rows_pad, ldw, m, l, y, f_out, R, alpha, n, t, coef);
+                                  int64_t r_rows, float* alpha, int64_t n, const int64_t* t,
+                                  float coef, hipStream_t s) {
+    hipLaunchKernelGGL(reduce_residual_kernel, dim3(blocks_for(r_rows * ldw)), dim3(256), 0, s,
+                       part, slices, rows_pad, ldw, m, l, y, f_out, R, r_rows, alpha, n, t, coef);
     return hipGetLastError();
 }
 

@@ -9,11 +9,13 @@
 // produced tile by tile in registers and contracted on the spot; it never
 // reaches global memory.
 //
-// Per workgroup (4 waves): a block of 64 query rows and a contiguous range of
-// centres (one "split"), walked 64 centres at a time.
+// One workgroup = 8 waves (two per SIMD) owns 64 query rows and a contiguous
+// range of centres (a "split"), walked 128 centres at a time:
 //   1. S = C_tile . Q_tile^T on fp32 MFMA (v_mfma_f32_32x32x2f32): each wave
-//      owns one 32x32 sub-tile; features stream through double-buffered LDS
-//      in chunks of 32.
+//      owns one 32x32 sub-tile of the 128 x 64 block. Features stream
+//      through two LDS slots in chunks of 32; the global loads of a chunk are
+//      issued two chunks ahead (across tile boundaries), so their latency
+//      hides behind two chunks of MFMA work.
 //   2. Epilogue in registers: d2 = |q|^2 + |c|^2 - 2 S, clamped at 0; then
 //      exp2(scale * d2) (Gaussian) or exp2(scale * sqrt(d2)) (Laplacian).
 //      Where the query and the centre are the same training point the value
@@ -21,9 +23,11 @@
 //   3. The kernel values go to LDS in the MFMA accumulator order, which is
 //      exactly the operand order the second product needs, and
 //      out^T(labels x queries) += W^T(labels x centres) . K(centres x queries)
-//      runs on the same MFMA with W read straight from global memory.
-// Partial sums of each split are written to their own slice and summed by a
-// separate deterministic reduction.
+//      runs on the same MFMA with W read straight from global memory (one
+//      step ahead). The label tiles are spread over the 8 waves so that the
+//      accumulators of up to 1024 labels fit in 128 registers per lane.
+// Partial sums of each split (and centre group, see wl/wj) are written to
+// their own slice and summed by a separate deterministic reduction.
 #include "ep_internal.h"
 
 #include <algorithm>
@@ -34,9 +38,13 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int kDC = 32;          // features per staged chunk
-constexpr int kLds = kDC + 4;    // padded LDS row (floats): conflict-free b128 reads
-constexpr int kMaxLtw = 8;       // label tiles per wave (accumulator budget)
+constexpr int kDC = 32;              // features per staged chunk
+constexpr int kLds = kDC + 4;        // padded LDS row (floats): conflict-free b128 reads
+constexpr int kRows = kBM + kBN;     // staged rows per chunk: queries, then centres
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
+
+static_assert(kBM == 64 && kBN == 128 && kThreads == 512, "staging map assumes 64 x 128, 512");
 
 // Row, inside a 32x32 tile, of accumulator element v held by `lane` for the
 // 32x32x2 f32 MFMA; the column is lane % 32. The same map gives the k index
@@ -50,21 +58,64 @@ __device__ __forceinline__ floatx16 mfma(float a, float b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float4 load4(const float* base, int64_t row, int64_t nrows,
-                                        int64_t ld, int64_t col, int64_t d, bool vec) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (row < nrows) {
-        const float* ptr = base + row * ld + col;
-        if (vec && col + 3 < d) {
-            v = *reinterpret_cast<const float4*>(ptr);
-        } else {
-            if (col < d) v.x = ptr[0];
-            if (col + 1 < d) v.y = ptr[1];
-            if (col + 2 < d) v.z = ptr[2];
-            if (col + 3 < d) v.w = ptr[3];
-        }
+// Buffer descriptor over [base, base + bytes): loads at offsets outside it
+// return zero, which provides the zero padding of ragged tiles in hardware.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+// A per-lane offset that no descriptor reaches (descriptor extents are
+// bounded by 2^30 bytes on the host): the load returns zero. Offsets are
+// split into a per-lane part (voffset) and a wave-uniform part (soffset,
+// held in a scalar register); a lane's voffset alone already decides
+// whether it is in range.
+constexpr int kOOB = 0x40000000;
+
+__device__ __forceinline__ float ld1(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+// Features col .. col+3 (col = col_lane + col_base) of the row at byte
+// offset row_off. VEC: d % 4 == 0 and rows 16-byte aligned, so the four are
+// all in or all out.
+template <bool VEC>
+__device__ __forceinline__ float4 load_feat4(__amdgpu_buffer_rsrc_t r, int row_off, int col_lane,
+                                             int col_base, int d) {
+    const int col = col_lane + col_base;
+    const int soff = col_base * 4;
+    if (VEC) {
+        const int voff = col < d ? row_off + col_lane * 4 : kOOB;
+        return __builtin_bit_cast(float4,
+                                  __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
     }
+    const int base = row_off + col_lane * 4;
+    float4 v;
+    v.x = ld1(r, col < d ? base : kOOB, soff);
+    v.y = ld1(r, col + 1 < d ? base + 4 : kOOB, soff);
+    v.z = ld1(r, col + 2 < d ? base + 8 : kOOB, soff);
+    v.w = ld1(r, col + 3 < d ? base + 12 : kOOB, soff);
     return v;
+}
+
+// LTW consecutive weights (one per virtual label tile).
+template <int LTW>
+__device__ __forceinline__ void load_w(__amdgpu_buffer_rsrc_t r, int voff, int soff, float* dst) {
+    if (LTW == 4) {
+        const float4 v = __builtin_bit_cast(
+            float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+        dst[0] = v.x;
+        dst[1] = v.y;
+        dst[2] = v.z;
+        dst[3] = v.w;
+    } else if (LTW == 2) {
+        const float2 v =
+            __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+        dst[0] = v.x;
+        dst[1] = v.y;
+    } else {
+#pragma unroll
+        for (int i = 0; i < LTW; ++i) dst[i] = ld1(r, voff == kOOB ? kOOB : voff + 4 * i, soff);
+    }
 }
 
 template <int KIND>
@@ -74,24 +125,30 @@ __device__ __forceinline__ float kernel_value(float d2, float scale) {
     return __builtin_amdgcn_exp2f(scale * __builtin_amdgcn_sqrtf(d2));
 }
 
-template <int KIND, int LTW>
-__global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p, int vec_ok) {
-    __shared__ __attribute__((aligned(16))) float xq[2][kBM][kLds];
-    __shared__ __attribute__((aligned(16))) float xc[2][kBN][kLds];
+// One thread's share of a staged chunk: query row lr, centre rows lr, 64+lr.
+struct Stage {
+    float4 q, c0, c1;
+};
+
+template <int KIND, int LTW, bool VEC, int PF>
+__global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
+    __shared__ __attribute__((aligned(16))) float xs[2][kRows][kLds];
     __shared__ float kb[kCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
-    __shared__ float s_cn[kBN];
     __shared__ int64_t s_qid[kBM];
-    __shared__ int64_t s_cid[kBN];
+    __shared__ float s_cn[2][kBN];
+    __shared__ int64_t s_cid[2][kBN];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int64_t q0 = (int64_t)blockIdx.x * kBM;
-    const int split = blockIdx.y;
-    const int64_t cb = (int64_t)split * p.cps;
+    const int64_t cb = (int64_t)blockIdx.y * p.cps;
     const int64_t ce = min(p.nc, cb + p.cps);
-    const bool vec = vec_ok != 0;
+    const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
+    const int nchunk = (int)((p.d + kDC - 1) / kDC);
+    const int64_t total = ntile * nchunk;
+    const int d = (int)p.d;
 
     if (tid < kBM) {
         const int64_t q = q0 + tid;
@@ -99,14 +156,25 @@ __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p, int vec_ok) {
         s_qn[tid] = ok ? p.qn[q] : 0.f;
         s_qid[tid] = (ok && p.qid) ? p.qid[q] : -1;
     }
+    auto load_centre_meta = [&](int64_t tile) {
+        if (tid < kBN) {
+            const int64_t c = cb + tile * kBN + tid;
+            const bool ok = c < ce;
+            s_cn[tile & 1][tid] = ok ? p.cn[c] : 0.f;
+            s_cid[tile & 1][tid] = ok ? (p.cid ? p.cid[c] : c) : -2;
+        }
+    };
+    if (ntile > 0) load_centre_meta(0);
 
-    // distance sub-tile of this wave
-    const int jt_s = wave >> 1;
-    const int bt_s = wave & 1;
-    // contraction role of this wave
-    const int gl = wave % p.wl;
+    const int qt_s = wave & 1;          // distance sub-tile of this wave
+    const int ct_s = wave >> 1;
+    const int gl = wave % p.wl;         // contraction role of this wave
     const int gj = wave / p.wl;
-    const bool active = wave < p.wl * p.wj;
+    // this wave's labels: a contiguous block of 32*LTW; lane m holds labels
+    // lb + LTW*m + i of its LTW virtual tiles i
+    const int lb = gl * LTW * kTile;
+    const int lvalid = p.lt * kTile;
+    const bool active = wave < p.wl * p.wj && lb < lvalid;
 
     floatx16 facc[LTW][kQSub];
 #pragma unroll
@@ -115,143 +183,194 @@ __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p, int vec_ok) {
         for (int b = 0; b < kQSub; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
-
-    const int lr = tid >> 3;          // staged row (0..31; +32 for the second half)
-    const int lc = (tid & 7) << 2;    // staged column inside the chunk
-    const int64_t nchunk = (p.d + kDC - 1) / kDC;
-
-    for (int64_t c0 = cb; c0 < ce; c0 += kBN) {
-        if (tid < kBN) {
-            const int64_t c = c0 + tid;
-            const bool ok = c < ce;
-            s_cn[tid] = ok ? p.cn[c] : 0.f;
-            s_cid[tid] = ok ? (p.cid ? p.cid[c] : c) : -2;
-        }
-        floatx16 sacc;
+    floatx16 sacc;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+    for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
 
-        float4 rq0 = load4(p.Q, q0 + lr, p.nq, p.ldq, lc, p.d, vec);
-        float4 rq1 = load4(p.Q, q0 + lr + 32, p.nq, p.ldq, lc, p.d, vec);
-        float4 rc0 = load4(p.C, c0 + lr, ce, p.ldc, lc, p.d, vec);
-        float4 rc1 = load4(p.C, c0 + lr + 32, ce, p.ldc, lc, p.d, vec);
-        *reinterpret_cast<float4*>(&xq[0][lr][lc]) = rq0;
-        *reinterpret_cast<float4*>(&xq[0][lr + 32][lc]) = rq1;
-        *reinterpret_cast<float4*>(&xc[0][lr][lc]) = rc0;
-        *reinterpret_cast<float4*>(&xc[0][lr + 32][lc]) = rc1;
-        __syncthreads();
+    const int lr = tid >> 3;
+    const int lc = (tid & 7) << 2;
+    const int64_t q_rows = min((int64_t)kBM, p.nq - q0);
+    const __amdgpu_buffer_rsrc_t qrs =
+        make_rsrc(p.Q + q0 * p.ldq, ((q_rows - 1) * p.ldq + p.d) * 4);
+    const int q_off = lr * (int)p.ldq * 4;
+    const int c_off0 = lr * (int)p.ldc * 4;
+    const int c_off1 = (lr + 64) * (int)p.ldc * 4;
 
-        for (int64_t ch = 0; ch < nchunk; ++ch) {
-            const int buf = (int)(ch & 1);
-            const bool more = ch + 1 < nchunk;
-            if (more) {
-                const int64_t k1 = (ch + 1) * kDC + lc;
-                rq0 = load4(p.Q, q0 + lr, p.nq, p.ldq, k1, p.d, vec);
-                rq1 = load4(p.Q, q0 + lr + 32, p.nq, p.ldq, k1, p.d, vec);
-                rc0 = load4(p.C, c0 + lr, ce, p.ldc, k1, p.d, vec);
-                rc1 = load4(p.C, c0 + lr + 32, ce, p.ldc, k1, p.d, vec);
-            }
-            // Lane (row = lane%32, half h = lane/32) reads features
-            // 8g+4h .. 8g+4h+3; step i of group g pairs feature 8g+i (lower
-            // half) with 8g+4+i (upper half). A and B use the same map, so
-            // every feature is contracted exactly once.
-            const float* arow = &xc[buf][jt_s * 32 + (lane & 31)][(lane >> 5) << 2];
-            const float* brow = &xq[buf][bt_s * 32 + (lane & 31)][(lane >> 5) << 2];
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const float4 a = *reinterpret_cast<const float4*>(arow + 8 * g);
-                const float4 b = *reinterpret_cast<const float4*>(brow + 8 * g);
-                sacc = mfma(a.x, b.x, sacc);
-                sacc = mfma(a.y, b.y, sacc);
-                sacc = mfma(a.z, b.z, sacc);
-                sacc = mfma(a.w, b.w, sacc);
-            }
-            if (more) {
-                *reinterpret_cast<float4*>(&xq[buf ^ 1][lr][lc]) = rq0;
-                *reinterpret_cast<float4*>(&xq[buf ^ 1][lr + 32][lc]) = rq1;
-                *reinterpret_cast<float4*>(&xc[buf ^ 1][lr][lc]) = rc0;
-                *reinterpret_cast<float4*>(&xc[buf ^ 1][lr + 32][lc]) = rc1;
-            }
-            __syncthreads();
+    int64_t pf_tile = 0;                // next chunk to fetch
+    int pf_ch = 0;
+    auto fetch = [&](Stage& s) {
+        const int64_t c0 = cb + pf_tile * kBN;
+        const __amdgpu_buffer_rsrc_t crs =
+            make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
+        const int kbase = pf_ch * kDC;
+        s.q = load_feat4<VEC>(qrs, q_off, lc, kbase, d);
+        s.c0 = load_feat4<VEC>(crs, c_off0, lc, kbase, d);
+        s.c1 = load_feat4<VEC>(crs, c_off1, lc, kbase, d);
+        if (++pf_ch == nchunk) {
+            pf_ch = 0;
+            ++pf_tile;
         }
+    };
+    auto stash = [&](int slot, const Stage& s) {
+        *reinterpret_cast<float4*>(&xs[slot][lr][lc]) = s.q;
+        *reinterpret_cast<float4*>(&xs[slot][kBM + lr][lc]) = s.c0;
+        *reinterpret_cast<float4*>(&xs[slot][kBM + 64 + lr][lc]) = s.c1;
+    };
 
-        // epilogue: distances -> kernel values, stored in accumulator order
-        {
-            const int bl = bt_s * 32 + (lane & 31);
+    // This lane's weights for k-step (jt, v) sit in row jt*32 + acc_row(v,
+    // lane) of the tile: the lane part (4 * half + column) goes in voffset,
+    // the rest (jt*32 + 8*(v/4) + v%4 rows) in soffset.
+    const int w_col = lb + LTW * (lane & 31);
+    const int ldw4 = (int)p.ldw * 4;
+    const int w_voff = w_col < lvalid ? ((lane >> 5) << 2) * ldw4 + w_col * 4 : kOOB;
+    auto w_soff = [&](int jt, int v) { return (jt * 32 + ((v >> 2) << 3) + (v & 3)) * ldw4; };
+
+    int64_t tile = 0;
+    int ch = 0;
+    // S += C_chunk . Q_chunk^T for the chunk staged in `slot`. Lane (row =
+    // lane%32, half h = lane/32) reads features 8g+4h .. 8g+4h+3; step i of
+    // group g pairs feature 8g+i (lower half) with 8g+4+i (upper half). A
+    // and B use the same map, so every feature is contracted exactly once.
+    auto chunk_mfma = [&](int slot) {
+        const float* arow = &xs[slot][kBM + ct_s * 32 + (lane & 31)][(lane >> 5) << 2];
+        const float* brow = &xs[slot][qt_s * 32 + (lane & 31)][(lane >> 5) << 2];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 a = *reinterpret_cast<const float4*>(arow + 8 * g);
+            const float4 b = *reinterpret_cast<const float4*>(brow + 8 * g);
+            sacc = mfma(a.x, b.x, sacc);
+            sacc = mfma(a.y, b.y, sacc);
+            sacc = mfma(a.z, b.z, sacc);
+            sacc = mfma(a.w, b.w, sacc);
+        }
+    };
+    // After the last chunk of a tile: kernel values, then the contraction.
+    auto finish_chunk = [&]() {
+        if (ch == nchunk - 1) {
+            // epilogue: distances -> kernel values, stored in accumulator order
+            const int64_t c0 = cb + tile * kBN;
+            const int bl = qt_s * 32 + (lane & 31);
             const float qnb = s_qn[bl];
             const int64_t qidb = s_qid[bl];
+            const float* cn = s_cn[tile & 1];
+            const int64_t* cid = s_cid[tile & 1];
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int jl = jt_s * 32 + acc_row(v, lane);
-                float kv = kernel_value<KIND>(qnb + s_cn[jl] - 2.f * sacc[v], p.scale);
-                if (qidb == s_cid[jl]) kv = 1.f;
+                const int jl = ct_s * 32 + acc_row(v, lane);
+                float kv = kernel_value<KIND>(qnb + cn[jl] - 2.f * sacc[v], p.scale);
+                if (qidb == cid[jl]) kv = 1.f;
                 if (c0 + jl >= ce) kv = 0.f;
-                kb[jt_s][bt_s][v][lane] = kv;
+                kb[ct_s][qt_s][v][lane] = kv;
+                sacc[v] = 0.f;
             }
-        }
-        __syncthreads();
+            if (tile + 1 < ntile) load_centre_meta(tile + 1);
+            __syncthreads();
 
-        // contraction: out^T[label, q] += W[c, label] * K[c, q]
-        if (active) {
-            for (int jt = gj; jt < kCSub; jt += p.wj) {
+            // contraction: out^T[label, q] += W[c, label] * K[c, q], with the
+            // W fragments of the next step in flight during this step's MFMAs
+            if (active) {
+                const __amdgpu_buffer_rsrc_t wrs =
+                    make_rsrc(p.W + c0 * p.ldw, (int64_t)kBN * p.ldw * 4);
+                float acur[LTW], anxt[LTW];
+                load_w<LTW>(wrs, w_voff, w_soff(gj, 0), acur);
+                for (int jt = gj; jt < kCSub; jt += p.wj) {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const float k0v = kb[jt][0][v][lane];
-                    const float k1v = kb[jt][1][v][lane];
-                    const int64_t wrow = c0 + jt * 32 + acc_row(v, lane);
-                    const float* wp = p.W + wrow * p.ldw + (lane & 31);
+                    for (int v = 0; v < 16; ++v) {
+                        if (v < 15)
+                            load_w<LTW>(wrs, w_voff, w_soff(jt, v + 1), anxt);
+                        else if (jt + p.wj < kCSub)
+                            load_w<LTW>(wrs, w_voff, w_soff(jt + p.wj, 0), anxt);
+                        const float k0v = kb[jt][0][v][lane];
+                        const float k1v = kb[jt][1][v][lane];
 #pragma unroll
-                    for (int i = 0; i < LTW; ++i) {
-                        const int lt = gl + i * p.wl;
-                        if (lt < p.lt) {
-                            const float a = wp[lt * 32];
-                            facc[i][0] = mfma(a, k0v, facc[i][0]);
-                            facc[i][1] = mfma(a, k1v, facc[i][1]);
+                        for (int i = 0; i < LTW; ++i) {
+                            facc[i][0] = mfma(acur[i], k0v, facc[i][0]);
+                            facc[i][1] = mfma(acur[i], k1v, facc[i][1]);
                         }
+#pragma unroll
+                        for (int i = 0; i < LTW; ++i) acur[i] = anxt[i];
                     }
                 }
             }
+            ++tile;
+            ch = 0;
+        } else {
+            ++ch;
         }
-        // The staging barrier of the next iteration orders these kb reads
-        // before the next epilogue overwrites kb.
+        // publishes the slot staged in this step and orders this chunk's
+        // reads of its slot before the next step overwrites it; also orders
+        // the kb reads above before the next epilogue writes kb
+        __syncthreads();
+    };
+
+    if (PF == 2) {
+        // chunk it+2 is fetched while chunk it is multiplied and chunk it+1
+        // (fetched one step earlier) is moved to LDS
+        Stage sa, sb;
+        if (total > 0) fetch(sa);
+        if (total > 1) fetch(sb);
+        if (total > 0) stash(0, sa);
+        __syncthreads();
+        auto step = [&](int64_t it, int slot, Stage& next_dst, const Stage& ready) {
+            if (it + 2 < total) fetch(next_dst);
+            chunk_mfma(slot);
+            if (it + 1 < total) stash(slot ^ 1, ready);
+            finish_chunk();
+        };
+        for (int64_t it = 0; it < total; it += 2) {
+            step(it, 0, sa, sb);
+            if (it + 1 < total) step(it + 1, 1, sb, sa);
+        }
+    } else {
+        // chunk it+1 is fetched while chunk it is multiplied
+        Stage st;
+        if (total > 0) {
+            fetch(st);
+            stash(0, st);
+        }
+        __syncthreads();
+        for (int64_t it = 0; it < total; ++it) {
+            const int slot = (int)(it & 1);
+            if (it + 1 < total) fetch(st);
+            chunk_mfma(slot);
+            if (it + 1 < total) stash(slot ^ 1, st);
+            finish_chunk();
+        }
     }
 
     if (active) {
-        const int slice = split * p.wj + gj;
+        const int slice = blockIdx.y * p.wj + gj;
         float* o = p.out + ((int64_t)slice * p.out_rows + q0) * p.ldw;
 #pragma unroll
-        for (int i = 0; i < LTW; ++i) {
-            const int lt = gl + i * p.wl;
-            if (lt < p.lt) {
+        for (int b = 0; b < kQSub; ++b) {
+            const int64_t row = b * 32 + (lane & 31);
 #pragma unroll
-                for (int b = 0; b < kQSub; ++b) {
-                    const int64_t row = b * 32 + (lane & 31);
+            for (int v = 0; v < 16; ++v) {
+                const int col = lb + LTW * acc_row(v, lane);
 #pragma unroll
-                    for (int v = 0; v < 16; ++v)
-                        o[row * p.ldw + lt * 32 + acc_row(v, lane)] = facc[i][b][v];
-                }
+                for (int i = 0; i < LTW; ++i)
+                    if (col + i < lvalid) o[row * p.ldw + col + i] = facc[i][b][v];
             }
         }
     }
 }
 
-typedef void (*KmvFn)(KmvArgs, int);
+typedef void (*KmvFn)(KmvArgs);
 
-template <int KIND>
+template <int KIND, bool VEC>
 KmvFn pick(int ltw) {
     switch (ltw) {
-        case 1: return kmv_kernel<KIND, 1>;
-        case 2: return kmv_kernel<KIND, 2>;
-        case 3: return kmv_kernel<KIND, 3>;
-        case 4: return kmv_kernel<KIND, 4>;
-        case 5: return kmv_kernel<KIND, 5>;
-        case 6: return kmv_kernel<KIND, 6>;
-        case 7: return kmv_kernel<KIND, 7>;
-        default: return kmv_kernel<KIND, 8>;
+        case 1: return kmv_kernel<KIND, 1, VEC, 2>;
+        case 2: return kmv_kernel<KIND, 2, VEC, 2>;
+        case 3: return kmv_kernel<KIND, 3, VEC, 2>;
+        default: return kmv_kernel<KIND, 4, VEC, 1>;
     }
 }
 
-KmvFn kernel_for(int kind, int ltw) { return kind == 0 ? pick<0>(ltw) : pick<1>(ltw); }
+KmvFn kernel_for(int kind, int ltw, bool vec) {
+    if (kind == 0) return vec ? pick<0, true>(ltw) : pick<0, false>(ltw);
+    return vec ? pick<1, true>(ltw) : pick<1, false>(ltw);
+}
 
 int occupancy_slots(int kind, int ltw) {
     static int cus = -1;
@@ -264,8 +383,8 @@ int occupancy_slots(int kind, int ltw) {
             cus = prop.multiProcessorCount;
     }
     int per = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw), kThreads, 0) !=
-            hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true), kThreads,
+                                                     0) != hipSuccess ||
         per < 1)
         per = 1;
     return per * cus;
@@ -282,9 +401,10 @@ float kernel_scale(int kind, float bandwidth) {
 
 KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices) {
     KmvPlan best{};
-    const int lt = (int)std::min<int64_t>(ldw / 32, 32);
-    // contraction layout: fewest MFMA items on the busiest wave
-    const int layouts[3][2] = {{4, 1}, {2, 2}, {1, 2}};
+    const int lt = (int)std::min<int64_t>(ldw / kTile, 32);
+    // contraction layout (label groups wl x centre groups wj = 8 waves):
+    // fewest MFMA steps on the busiest wave, then fewest slices
+    const int layouts[3][2] = {{8, 1}, {4, 2}, {2, 4}};
     int best_cost = 1 << 30;
     for (auto& lw : layouts) {
         const int wl = lw[0], wj = lw[1];
@@ -327,17 +447,17 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s) {
     a.splits = p.splits;
     a.wl = p.wl;
     a.wj = p.wj;
-    const int vec_ok = ((a.ldq & 3) == 0) && ((a.ldc & 3) == 0) &&
-                       ((reinterpret_cast<uintptr_t>(a.Q) & 15) == 0) &&
-                       ((reinterpret_cast<uintptr_t>(a.C) & 15) == 0);
+    const bool vec = (a.d % 4 == 0) && ((a.ldq & 3) == 0) && ((a.ldc & 3) == 0) &&
+                     ((reinterpret_cast<uintptr_t>(a.Q) & 15) == 0) &&
+                     ((reinterpret_cast<uintptr_t>(a.C) & 15) == 0);
     dim3 grid((unsigned)ceil_div(std::max<int64_t>(a.nq, 1), kBM), (unsigned)p.splits);
     const int lt_total = a.lt;
     for (int t0 = 0; t0 < lt_total; t0 += 32) {
         KmvArgs b = a;
-        b.W = a.W + (int64_t)t0 * 32;
-        b.out = a.out + (int64_t)t0 * 32;
+        b.W = a.W + (int64_t)t0 * kTile;
+        b.out = a.out + (int64_t)t0 * kTile;
         b.lt = std::min(32, lt_total - t0);
-        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw), grid, dim3(kThreads), 0, s, b, vec_ok);
+        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec), grid, dim3(kThreads), 0, s, b);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

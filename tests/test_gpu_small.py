@@ -124,3 +124,36 @@ def test_error_paths_and_alpha_roundtrip():
         assert ei.value.code == ep.EP_EINVAL
         # empty prediction is a no-op
         ep.ep_predict(g.ctx, g.t(X[:1]), 0, torch.empty((1, l), device="cuda:0"))
+
+
+@pytest.mark.gpu
+def test_restore_from_saved_setup():
+    import paper_1806_06144_amd as ep
+    n, d, l, s, k = 900, 20, 6, 150, 15
+    X, Y, a0, rng = _problem(n, d, l, 4)
+    r = rng.choice(n, s, replace=False)
+    t = _batch(rng, n, r, 100)
+    with Gpu(X, l, "laplacian", 1.3, s, k, r) as g:
+        sigma, D, V, r_back = g.preconditioner()
+        g.set_alpha(a0)
+        F1 = g.step(t, Y[t])
+        a1 = g.alpha()
+        ctx2, info2 = ep.ep_restore(g.Xd, n, d, l, "laplacian", 1.3, s, k, r_back, sigma, V)
+        try:
+            assert info2.beta == pytest.approx(g.info.beta, rel=1e-6)
+            assert info2.m == g.info.m
+            sigma2, D2, V2, r2 = ep.ep_get_preconditioner(ctx2, info2)
+            np.testing.assert_array_equal(V2, V)
+            np.testing.assert_array_equal(D2, D)
+            ep.ep_set_alpha(ctx2, g.t(a0))
+            F2 = g.torch.empty((len(t), l), dtype=g.torch.float32, device=g.dev)
+            ep.ep_step(ctx2, g.t(t), len(t), g.t(Y[t]), F2)
+            a2 = g.torch.empty((n, l), dtype=g.torch.float32, device=g.dev)
+            ep.ep_get_alpha(ctx2, a2)
+            ep.ep_sync(ctx2)
+        finally:
+            ep.ep_destroy(ctx2)
+    np.testing.assert_array_equal(F2.cpu().numpy(), F1)
+    assert rel(a2.cpu().numpy() - a0, a1 - a0) < 1e-6
+    with pytest.raises(ep.EigenProError):
+        ep.ep_restore(g.Xd, n, d, l, "laplacian", 1.3, s, k, r_back, sigma[::-1].copy(), V)
