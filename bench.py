@@ -98,6 +98,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--s", type=int, default=None,
                     help="override the subsample size (experiments only)")
+    ap.add_argument("--shard", type=int, default=1,
+                    help="run one GPU's share of a G-way split of the centres: the "
+                         "first n/G rows of the same workload")
     ap.add_argument("--save-setup", default=None,
                     help="write the subsample and eigensystem to this .npz")
     ap.add_argument("--load-setup", default=None,
@@ -117,6 +120,8 @@ def main():
     cfg = synth.get_config(args.config)
     if args.s is not None:
         cfg = synth.get_config(args.config, s=args.s)
+    if args.shard > 1:
+        cfg = synth.get_config(args.config, n=cfg.n // args.shard, s=cfg.s)
     dev = torch.device("cuda:0")
     log(f"workload {cfg.name}: n={cfg.n} d={cfg.d} l={cfg.l} s={cfg.s} k={cfg.k}")
     t0 = time.perf_counter()
@@ -171,6 +176,8 @@ def main():
     kmv_avg_s = tim.kmv_ms / 1e3 / max(tim.kmv_launches, 1)
     achieved = kmv_flops / kmv_avg_s / 1e12
     workload = f"{cfg.name}-shaped n={n} d={d} l={l} {cfg.kernel} bw={cfg.bandwidth:g} s={s} k={k} m={m}"
+    if args.shard > 1:
+        workload += f" (1/{args.shard} centre shard)"
 
     if args.calibrate_copy:
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)

@@ -145,7 +145,8 @@ int record(hipStream_t s, std::vector<TimedPair>& v, bool start) {
 // is the caller's; returns the slice count in *slices.
 int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
             int64_t nq, const float* C, int64_t ldc, const float* cn, const int64_t* cid,
-            int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed) {
+            int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed,
+            bool subsample) {
     *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
     KmvPlan plan = kmv_plan(nq, nc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
     *slices = plan.slices();
@@ -173,7 +174,7 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
         int rc = record(c->stream, c->kmv_ev, true);
         if (rc) return rc;
     }
-    HIP_TRY(kmv_launch(a, plan, c->stream));
+    HIP_TRY(kmv_launch(a, plan, c->stream, subsample));
     if (timed) {
         int rc = record(c->stream, c->kmv_ev, false);
         if (rc) return rc;
@@ -498,7 +499,7 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     int slices = 0;
     int64_t rows_pad = 0;
     rc = run_kmv(c, xb, c->d, xbn, t, m, c->X, c->d, c->norms.as<float>(), nullptr, c->n, alpha,
-                 &slices, &rows_pad, c->timing);
+                 &slices, &rows_pad, c->timing, false);
     if (rc) return rc;
     // step 3: R = F - y_b; alpha_t -= c R
     const double coef = 1.0 / (c->info.beta + (double)(m - 1) * c->info.lambda_k1);
@@ -507,7 +508,7 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     if (c->k > 0) {
         // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
         rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(), c->r_dev.as<int64_t>(),
-                     c->s, xb, c->d, xbn, t, m, R, &slices, &rows_pad, false);
+                     c->s, xb, c->d, xbn, t, m, R, &slices, &rows_pad, false, true);
         if (rc) return rc;
         HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
         HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s, c->l_pad,
@@ -550,7 +551,7 @@ int ep_predict(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
         int64_t rows_pad = 0;
         int rc = run_kmv(c, Zc, c->d, c->zn.as<float>(), nullptr, nz, c->X, c->d,
                          c->norms.as<float>(), nullptr, c->n, c->alpha.as<float>(), &slices,
-                         &rows_pad, false);
+                         &rows_pad, false, false);
         if (rc) return rc;
         HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, nz, c->l,
                                    out + z0 * c->l, c->l, st));

@@ -54,8 +54,10 @@ struct KmvPlan {
     int slices() const { return splits * wj; }
 };
 KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices);
-// Launches one fused pass per block of up to 1024 label columns.
-hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s);
+// Launches one fused pass per block of up to 1024 label columns. `subsample`
+// selects the entry point used for the subsample pass (same code, its own
+// symbol in profiles).
+hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample);
 
 float kernel_scale(int kind, float bandwidth);
 

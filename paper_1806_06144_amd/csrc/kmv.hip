@@ -41,7 +41,6 @@ namespace {
 constexpr int kDC = 32;              // features per staged chunk
 constexpr int kLds = kDC + 4;        // padded LDS row (floats): conflict-free b128 reads
 constexpr int kRows = kBM + kBN;     // staged rows per chunk: queries, then centres
-constexpr int kWaves = kThreads / 64;
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
 
 static_assert(kBM == 64 && kBN == 128 && kThreads == 512, "staging map assumes 64 x 128, 512");
@@ -131,7 +130,7 @@ struct Stage {
 };
 
 template <int KIND, int LTW, bool VEC, int PF>
-__global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
+__device__ __forceinline__ void kmv_body(const KmvArgs& p) {
     __shared__ __attribute__((aligned(16))) float xs[2][kRows][kLds];
     __shared__ float kb[kCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
@@ -142,8 +141,14 @@ __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t q0 = (int64_t)blockIdx.x * kBM;
-    const int64_t cb = (int64_t)blockIdx.y * p.cps;
+    // query tiles run fastest: the 8 XCDs take launch slots round robin, so
+    // each XCD holds a block of query tiles x centre splits whose X rows,
+    // batch rows and weights it shares through its L2
+    const int tq = (int)((p.nq + kBM - 1) / kBM);
+    const int split = (int)blockIdx.x / tq;
+    const int qtile = (int)blockIdx.x - split * tq;
+    const int64_t q0 = (int64_t)qtile * kBM;
+    const int64_t cb = (int64_t)split * p.cps;
     const int64_t ce = min(p.nc, cb + p.cps);
     const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
     const int nchunk = (int)((p.d + kDC - 1) / kDC);
@@ -339,7 +344,7 @@ __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
     }
 
     if (active) {
-        const int slice = blockIdx.y * p.wj + gj;
+        const int slice = split * p.wj + gj;
         float* o = p.out + ((int64_t)slice * p.out_rows + q0) * p.ldw;
 #pragma unroll
         for (int b = 0; b < kQSub; ++b) {
@@ -355,21 +360,32 @@ __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
     }
 }
 
+// Two entry points with one body, so that profiles tell the predictions pass
+// (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
+template <int KIND, int LTW, bool VEC, int PF>
+__global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
+    kmv_body<KIND, LTW, VEC, PF>(p);
+}
+template <int KIND, int LTW, bool VEC, int PF>
+__global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
+    kmv_body<KIND, LTW, VEC, PF>(p);
+}
+
 typedef void (*KmvFn)(KmvArgs);
 
 template <int KIND, bool VEC>
-KmvFn pick(int ltw) {
+KmvFn pick(int ltw, bool sub) {
     switch (ltw) {
-        case 1: return kmv_kernel<KIND, 1, VEC, 2>;
-        case 2: return kmv_kernel<KIND, 2, VEC, 2>;
-        case 3: return kmv_kernel<KIND, 3, VEC, 2>;
-        default: return kmv_kernel<KIND, 4, VEC, 1>;
+        case 1: return sub ? kmv_subsample_kernel<KIND, 1, VEC, 2> : kmv_kernel<KIND, 1, VEC, 2>;
+        case 2: return sub ? kmv_subsample_kernel<KIND, 2, VEC, 2> : kmv_kernel<KIND, 2, VEC, 2>;
+        case 3: return sub ? kmv_subsample_kernel<KIND, 3, VEC, 2> : kmv_kernel<KIND, 3, VEC, 2>;
+        default: return sub ? kmv_subsample_kernel<KIND, 4, VEC, 1> : kmv_kernel<KIND, 4, VEC, 1>;
     }
 }
 
-KmvFn kernel_for(int kind, int ltw, bool vec) {
-    if (kind == 0) return vec ? pick<0, true>(ltw) : pick<0, false>(ltw);
-    return vec ? pick<1, true>(ltw) : pick<1, false>(ltw);
+KmvFn kernel_for(int kind, int ltw, bool vec, bool sub) {
+    if (kind == 0) return vec ? pick<0, true>(ltw, sub) : pick<0, false>(ltw, sub);
+    return vec ? pick<1, true>(ltw, sub) : pick<1, false>(ltw, sub);
 }
 
 int occupancy_slots(int kind, int ltw) {
@@ -383,8 +399,8 @@ int occupancy_slots(int kind, int ltw) {
             cus = prop.multiProcessorCount;
     }
     int per = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true), kThreads,
-                                                     0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true, false),
+                                                     kThreads, 0) != hipSuccess ||
         per < 1)
         per = 1;
     return per * cus;
@@ -442,7 +458,7 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices) 
     return best;
 }
 
-hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s) {
+hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample) {
     a.cps = p.cps;
     a.splits = p.splits;
     a.wl = p.wl;
@@ -450,14 +466,16 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s) {
     const bool vec = (a.d % 4 == 0) && ((a.ldq & 3) == 0) && ((a.ldc & 3) == 0) &&
                      ((reinterpret_cast<uintptr_t>(a.Q) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(a.C) & 15) == 0);
-    dim3 grid((unsigned)ceil_div(std::max<int64_t>(a.nq, 1), kBM), (unsigned)p.splits);
+    const int64_t tq = ceil_div(std::max<int64_t>(a.nq, 1), kBM);
+    dim3 grid((unsigned)(tq * p.splits));
     const int lt_total = a.lt;
     for (int t0 = 0; t0 < lt_total; t0 += 32) {
         KmvArgs b = a;
         b.W = a.W + (int64_t)t0 * kTile;
         b.out = a.out + (int64_t)t0 * kTile;
         b.lt = std::min(32, lt_total - t0);
-        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec), grid, dim3(kThreads), 0, s, b);
+        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec, subsample), grid, dim3(kThreads), 0, s,
+                           b);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
