@@ -187,6 +187,9 @@ def main():
         torch.cuda.synchronize()
         log("calibration copy: 3 x 1 GiB device-to-device")
 
+    probe_tf, probe_mhz = ep.ep_device_probe()
+    log(f"device probe: fp32 MFMA {probe_tf:.1f} TFLOP/s sustained at {probe_mhz:.0f} MHz")
+
     cpu = None
     if not args.no_cpu_baseline:
         alpha = torch.empty((n, l), dtype=torch.float32, device=dev)
@@ -227,6 +230,9 @@ def main():
             "avg_launch_ms": kmv_avg_s * 1e3,
             "launches": int(tim.kmv_launches),
             "flops_per_launch": kmv_flops,
+            "probe_mfma_f32_tflops": probe_tf,
+            "probe_shader_clock_mhz": probe_mhz,
+            "frac_of_probe": achieved / probe_tf if probe_tf > 0 else None,
         },
         "cpu_baseline": cpu,
     }

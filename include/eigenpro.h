@@ -163,6 +163,14 @@ typedef struct ep_timing {
 int ep_timing_enable(ep_ctx* ctx, int on);
 int ep_timing_read(ep_ctx* ctx, ep_timing* out);
 
+/* Device probe (no context): runs a register-only kernel of independent
+ * fp32 MFMA chains (v_mfma_f32_32x32x2f32, two waves per SIMD on every CU)
+ * on the current device and default stream, and reports the rate it
+ * sustains in TFLOP/s and the shader clock during it in MHz (ratio of the
+ * shader cycle counter to the 100 MHz constant counter). Blocking; about
+ * 0.1 s. Either out-pointer may be NULL. Errors: EP_EDEVICE, EP_ENOMEM. */
+int ep_device_probe(double* mfma_f32_tflops, double* shader_clock_mhz);
+
 /* Wait for all work of the context; reports deferred device errors
  * (EP_EDEVICE) and out-of-range batch indices seen since the last call
  * (EP_EINDEX). */

@@ -12,7 +12,9 @@ import os
 import re
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libeigenpro.so")
+# EIGENPRO_LIB selects another build of the same library (e.g. to compare
+# kernel variants); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("EIGENPRO_LIB") or os.path.join(_HERE, "libeigenpro.so")
 HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "eigenpro.h")
 
 EP_OK, EP_EINVAL, EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC, EP_EINDEX = 0, -1, -2, -3, -4, -5
@@ -70,6 +72,7 @@ def _load():
         "ep_timing_enable": (I, [P, I]),
         "ep_timing_read": (I, [P, ctypes.POINTER(EpTiming)]),
         "ep_sync": (I, [P]),
+        "ep_device_probe": (I, [P, P]),
         "ep_destroy": (None, [P]),
         "ep_last_error": (ctypes.c_char_p, []),
     }
@@ -225,6 +228,14 @@ def ep_timing_read(ctx):
     t = EpTiming()
     _check(_lib.ep_timing_read(ctx, ctypes.byref(t)))
     return t
+
+
+def ep_device_probe():
+    """(sustained fp32 MFMA TFLOP/s, shader clock MHz) of the current device."""
+    tf = ctypes.c_double()
+    mhz = ctypes.c_double()
+    _check(_lib.ep_device_probe(ctypes.byref(tf), ctypes.byref(mhz)))
+    return tf.value, mhz.value
 
 
 def ep_sync(ctx):

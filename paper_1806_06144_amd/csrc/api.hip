@@ -1,6 +1,6 @@
 // C ABI of libeigenpro: context, argument checking, buffer management and the
 // launch sequence of one EigenPro 2.0 iteration (Algorithm 1) on one GPU.
-#include "../../include/eigenpro.h"
+#include "eigenpro.h"
 #include "ep_internal.h"
 
 #include <rocblas/rocblas.h>

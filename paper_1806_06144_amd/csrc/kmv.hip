@@ -38,8 +38,6 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int kDC = 32;              // features per staged chunk
-constexpr int kLds = kDC + 4;        // padded LDS row (floats): conflict-free b128 reads
 constexpr int kRows = kBM + kBN;     // staged rows per chunk: queries, then centres
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
 
@@ -124,13 +122,20 @@ __device__ __forceinline__ float kernel_value(float d2, float scale) {
     return __builtin_amdgcn_exp2f(scale * __builtin_amdgcn_sqrtf(d2));
 }
 
-// One thread's share of a staged chunk: query row lr, centre rows lr, 64+lr.
+// One thread's share of a staged chunk of DC features: NP passes of
+// 512 / (DC/4) rows each over the 64 query rows then the 128 centre rows.
+template <int DC>
 struct Stage {
-    float4 q, c0, c1;
+    static constexpr int kCols = DC / 4;              // float4 per staged row
+    static constexpr int kRowsPerPass = kThreads / kCols;
+    static constexpr int kPasses = kRows / kRowsPerPass;
+    float4 v[kPasses];
 };
 
-template <int KIND, int LTW, bool VEC, int PF>
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
+    constexpr int kLds = DC + 4;     // padded LDS row (floats): conflict-free b128 reads
+    using St = Stage<DC>;
     __shared__ __attribute__((aligned(16))) float xs[2][kRows][kLds];
     __shared__ float kb[kCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
@@ -151,7 +156,7 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
     const int64_t cb = (int64_t)split * p.cps;
     const int64_t ce = min(p.nc, cb + p.cps);
     const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
-    const int nchunk = (int)((p.d + kDC - 1) / kDC);
+    const int nchunk = (int)((p.d + DC - 1) / DC);
     const int64_t total = ntile * nchunk;
     const int d = (int)p.d;
 
@@ -188,38 +193,48 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
         for (int b = 0; b < kQSub; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
-    floatx16 sacc;
+    // distance accumulator(s): with ACC2 alternate k-steps go to two
+    // independent accumulators, summed in the epilogue
+    floatx16 sacc, sacc2;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+    for (int v = 0; v < 16; ++v) {
+        sacc[v] = 0.f;
+        sacc2[v] = 0.f;
+    }
 
-    const int lr = tid >> 3;
-    const int lc = (tid & 7) << 2;
+    const int lr = tid / St::kCols;             // row inside a pass
+    const int lc = (tid % St::kCols) * 4;       // feature inside the chunk
     const int64_t q_rows = min((int64_t)kBM, p.nq - q0);
     const __amdgpu_buffer_rsrc_t qrs =
         make_rsrc(p.Q + q0 * p.ldq, ((q_rows - 1) * p.ldq + p.d) * 4);
-    const int q_off = lr * (int)p.ldq * 4;
-    const int c_off0 = lr * (int)p.ldc * 4;
-    const int c_off1 = (lr + 64) * (int)p.ldc * 4;
+    // byte offset of this thread's row in each pass (query rows first)
+    int row_off[St::kPasses];
+#pragma unroll
+    for (int ps = 0; ps < St::kPasses; ++ps) {
+        const int sr = ps * St::kRowsPerPass;
+        row_off[ps] = sr < kBM ? (sr + lr) * (int)p.ldq * 4 : (sr - kBM + lr) * (int)p.ldc * 4;
+    }
 
     int64_t pf_tile = 0;                // next chunk to fetch
     int pf_ch = 0;
-    auto fetch = [&](Stage& s) {
+    auto fetch = [&](St& s) {
         const int64_t c0 = cb + pf_tile * kBN;
         const __amdgpu_buffer_rsrc_t crs =
             make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
-        const int kbase = pf_ch * kDC;
-        s.q = load_feat4<VEC>(qrs, q_off, lc, kbase, d);
-        s.c0 = load_feat4<VEC>(crs, c_off0, lc, kbase, d);
-        s.c1 = load_feat4<VEC>(crs, c_off1, lc, kbase, d);
+        const int kbase = pf_ch * DC;
+#pragma unroll
+        for (int ps = 0; ps < St::kPasses; ++ps)
+            s.v[ps] = load_feat4<VEC>(ps * St::kRowsPerPass < kBM ? qrs : crs, row_off[ps], lc,
+                                      kbase, d);
         if (++pf_ch == nchunk) {
             pf_ch = 0;
             ++pf_tile;
         }
     };
-    auto stash = [&](int slot, const Stage& s) {
-        *reinterpret_cast<float4*>(&xs[slot][lr][lc]) = s.q;
-        *reinterpret_cast<float4*>(&xs[slot][kBM + lr][lc]) = s.c0;
-        *reinterpret_cast<float4*>(&xs[slot][kBM + 64 + lr][lc]) = s.c1;
+    auto stash = [&](int slot, const St& s) {
+#pragma unroll
+        for (int ps = 0; ps < St::kPasses; ++ps)
+            *reinterpret_cast<float4*>(&xs[slot][ps * St::kRowsPerPass + lr][lc]) = s.v[ps];
     };
 
     // This lane's weights for k-step (jt, v) sit in row jt*32 + acc_row(v,
@@ -240,13 +255,20 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
         const float* arow = &xs[slot][kBM + ct_s * 32 + (lane & 31)][(lane >> 5) << 2];
         const float* brow = &xs[slot][qt_s * 32 + (lane & 31)][(lane >> 5) << 2];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < DC / 8; ++g) {
             const float4 a = *reinterpret_cast<const float4*>(arow + 8 * g);
             const float4 b = *reinterpret_cast<const float4*>(brow + 8 * g);
-            sacc = mfma(a.x, b.x, sacc);
-            sacc = mfma(a.y, b.y, sacc);
-            sacc = mfma(a.z, b.z, sacc);
-            sacc = mfma(a.w, b.w, sacc);
+            if (ACC2) {
+                sacc = mfma(a.x, b.x, sacc);
+                sacc2 = mfma(a.y, b.y, sacc2);
+                sacc = mfma(a.z, b.z, sacc);
+                sacc2 = mfma(a.w, b.w, sacc2);
+            } else {
+                sacc = mfma(a.x, b.x, sacc);
+                sacc = mfma(a.y, b.y, sacc);
+                sacc = mfma(a.z, b.z, sacc);
+                sacc = mfma(a.w, b.w, sacc);
+            }
         }
     };
     // After the last chunk of a tile: kernel values, then the contraction.
@@ -262,11 +284,13 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int jl = ct_s * 32 + acc_row(v, lane);
-                float kv = kernel_value<KIND>(qnb + cn[jl] - 2.f * sacc[v], p.scale);
+                const float dot = ACC2 ? sacc[v] + sacc2[v] : sacc[v];
+                float kv = kernel_value<KIND>(qnb + cn[jl] - 2.f * dot, p.scale);
                 if (qidb == cid[jl]) kv = 1.f;
                 if (c0 + jl >= ce) kv = 0.f;
                 kb[ct_s][qt_s][v][lane] = kv;
                 sacc[v] = 0.f;
+                sacc2[v] = 0.f;
             }
             if (tile + 1 < ntile) load_centre_meta(tile + 1);
             __syncthreads();
@@ -308,38 +332,27 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
         __syncthreads();
     };
 
-    if (PF == 2) {
-        // chunk it+2 is fetched while chunk it is multiplied and chunk it+1
-        // (fetched one step earlier) is moved to LDS
-        Stage sa, sb;
-        if (total > 0) fetch(sa);
-        if (total > 1) fetch(sb);
-        if (total > 0) stash(0, sa);
-        __syncthreads();
-        auto step = [&](int64_t it, int slot, Stage& next_dst, const Stage& ready) {
-            if (it + 2 < total) fetch(next_dst);
-            chunk_mfma(slot);
-            if (it + 1 < total) stash(slot ^ 1, ready);
-            finish_chunk();
-        };
-        for (int64_t it = 0; it < total; it += 2) {
-            step(it, 0, sa, sb);
-            if (it + 1 < total) step(it + 1, 1, sb, sa);
-        }
-    } else {
-        // chunk it+1 is fetched while chunk it is multiplied
-        Stage st;
-        if (total > 0) {
-            fetch(st);
-            stash(0, st);
-        }
-        __syncthreads();
-        for (int64_t it = 0; it < total; ++it) {
-            const int slot = (int)(it & 1);
-            if (it + 1 < total) fetch(st);
-            chunk_mfma(slot);
-            if (it + 1 < total) stash(slot ^ 1, st);
-            finish_chunk();
+    // PF register stages rotate: at step it, stage it % PF (whose chunk was
+    // moved to LDS one step earlier) receives the loads of chunk it + PF,
+    // and stage (it+1) % PF, loaded PF-1 steps earlier, is moved to LDS for
+    // the next step.
+    St st[PF];
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+        if (j < total) fetch(st[j]);
+    if (total > 0) stash(0, st[0]);
+    __syncthreads();
+    for (int64_t it0 = 0; it0 < total; it0 += PF) {
+#pragma unroll
+        for (int j = 0; j < PF; ++j) {
+            const int64_t it = it0 + j;
+            if (it < total) {
+                const int slot = (int)(it & 1);
+                if (it + PF < total) fetch(st[j]);
+                chunk_mfma(slot);
+                if (it + 1 < total) stash(slot ^ 1, st[(j + 1) % PF]);
+                finish_chunk();
+            }
         }
     }
 
@@ -362,13 +375,13 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
 
 // Two entry points with one body, so that profiles tell the predictions pass
 // (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
-template <int KIND, int LTW, bool VEC, int PF>
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
-    kmv_body<KIND, LTW, VEC, PF>(p);
+    kmv_body<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
-template <int KIND, int LTW, bool VEC, int PF>
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
-    kmv_body<KIND, LTW, VEC, PF>(p);
+    kmv_body<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 
 typedef void (*KmvFn)(KmvArgs);
@@ -376,10 +389,10 @@ typedef void (*KmvFn)(KmvArgs);
 template <int KIND, bool VEC>
 KmvFn pick(int ltw, bool sub) {
     switch (ltw) {
-        case 1: return sub ? kmv_subsample_kernel<KIND, 1, VEC, 2> : kmv_kernel<KIND, 1, VEC, 2>;
-        case 2: return sub ? kmv_subsample_kernel<KIND, 2, VEC, 2> : kmv_kernel<KIND, 2, VEC, 2>;
-        case 3: return sub ? kmv_subsample_kernel<KIND, 3, VEC, 2> : kmv_kernel<KIND, 3, VEC, 2>;
-        default: return sub ? kmv_subsample_kernel<KIND, 4, VEC, 1> : kmv_kernel<KIND, 4, VEC, 1>;
+        case 1: return sub ? kmv_subsample_kernel<KIND, 1, VEC, 2, 32, true> : kmv_kernel<KIND, 1, VEC, 2, 32, true>;
+        case 2: return sub ? kmv_subsample_kernel<KIND, 2, VEC, 2, 64, true> : kmv_kernel<KIND, 2, VEC, 2, 64, true>;
+        case 3: return sub ? kmv_subsample_kernel<KIND, 3, VEC, 1, 64, false> : kmv_kernel<KIND, 3, VEC, 1, 64, false>;
+        default: return sub ? kmv_subsample_kernel<KIND, 4, VEC, 1, 32, false> : kmv_kernel<KIND, 4, VEC, 1, 32, false>;
     }
 }
 
