@@ -57,6 +57,12 @@ typedef struct ep_info {
                            step moves each coordinate by eta/m times its
                            residual                                          */
     double setup_ms;    /* wall time of ep_setup                              */
+    int64_t k_max;      /* rank of the eigensystem held (the k of ep_setup);
+                           the active rank k can be lowered to any value
+                           <= k_max without a new eigensolve (ep_set_rank,
+                           ep_adapt)                                         */
+    double accel;       /* after ep_adapt: beta(K)/beta(K_G) * m_G / m*(k),
+                           the acceleration of Section 3's claim (0 before)  */
 } ep_info;
 
 /*
@@ -145,6 +151,37 @@ int ep_get_preconditioner(ep_ctx* ctx, double* sigma, double* D, float* V,
                           int64_t* r);
 
 int ep_get_info(ep_ctx* ctx, ep_info* info);
+
+/*
+ * Resource-adaptive parameters (Section 3, Steps 1-3).
+ *
+ * ep_set_rank(ctx, k): make rank k (0 <= k <= info.k_max) the active
+ *   preconditioner: V keeps its top k columns, D, beta(K_G), lambda =
+ *   sigma_{k+1}/s, m* and the step size are recomputed from the held
+ *   eigensystem (no new eigensolve). Errors: EP_EINVAL.
+ * ep_adapt(ctx, m_G, info): Step 2 / Eq. 7 — choose the largest rank k <=
+ *   k_max whose adapted kernel has critical batch m*(k) = beta(k) s /
+ *   sigma_{k+1} <= m_G, make it active, and (Step 3) set the batch to
+ *   min(n, m_G) with its step size; info.accel gets the acceleration
+ *   beta(K)/beta(K_G) * m_G / m*(k) of the original kernel's m*(k) = s /
+ *   sigma_1. Errors: EP_EINVAL (m_G < 1).
+ * ep_batch_sweep(ctx, ms, count, reps, ms_per_pass): times the step-2
+ *   fused pass (the first ms[i] rows of X as the batch, against all n
+ *   centres, current alpha) for each batch size, averaged over reps launches,
+ *   in ms (host array of count doubles). Synchronises. Errors: EP_EINVAL.
+ * ep_resource_batch(ctx, tol, m_C, m_S, m_G): Step 1. m_S = the batch at
+ *   which the paper's memory model (d + l + m) n floats fills the device's
+ *   memory; m_C = the smallest power-of-two batch (32 .. 32768) whose
+ *   measured kernel-entry throughput is within tol of the best, i.e. where
+ *   time per step stops being flat; m_G = min(m_C, m_S). Any output may be
+ *   NULL. Synchronises. Errors: EP_EINVAL (tol outside (0, 1)).
+ */
+int ep_set_rank(ep_ctx* ctx, int64_t k);
+int ep_adapt(ep_ctx* ctx, int64_t m_G, ep_info* info);
+int ep_batch_sweep(ep_ctx* ctx, const int64_t* ms, int count, int reps,
+                   double* ms_per_pass);
+int ep_resource_batch(ep_ctx* ctx, double tol, int64_t* m_C, int64_t* m_S,
+                      int64_t* m_G);
 
 /* Enable (1) / disable (0, default) host-side validation of batch indices
  * in ep_step (copies t to the host and synchronises). */

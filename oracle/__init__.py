@@ -23,6 +23,9 @@ from .eigenpro import (
     predict,
     run_epoch,
     interpolant,
+    with_rank,
+    choose_rank,
+    acceleration,
 )
 
 __all__ = [
@@ -39,4 +42,7 @@ __all__ = [
     "predict",
     "run_epoch",
     "interpolant",
+    "with_rank",
+    "choose_rank",
+    "acceleration",
 ]

@@ -27,6 +27,11 @@ step_pointwise     Algorithm 1, steps 2-5, one point and one coordinate at a
 predict            Section 2: f(z) = sum_i alpha_i k(x_i, z).
 interpolant        Section 2: alpha* = K^{-1} y, the unique interpolating
                    solution every iteration converges to.
+with_rank          Section 3 Step 2 / Section 4: the adapted kernel of a lower
+                   rank k' from the same eigensystem.
+choose_rank        Section 3 Step 2, Eq. 7: the largest rank whose critical
+                   batch does not exceed the resource batch m_G.
+acceleration       Section 3 claim: beta(K)/beta(K_G) * m_G / m*(k).
 
 Readings of the paper (shared with the HIP path by construction)
 ----------------------------------------------------------------
@@ -242,3 +247,36 @@ def interpolant(X, Y, kernel, bandwidth):
     """alpha* = K^{-1} Y (Section 2), by a dense solve."""
     K = kernel_matrix(X, X, kernel, bandwidth)
     return np.linalg.solve(K, _f64(Y))
+
+
+def with_rank(state, k):
+    """The same subsample and eigensystem flattened at rank k <= state.k:
+    V keeps its top k columns, sigma_{k+1} becomes the floor, and beta, m*,
+    m are recomputed (Section 3 Step 2, Section 4)."""
+    if not 0 <= k <= state.k:
+        raise ValueError("rank outside [0, k]")
+    sigma = state.sigma[:k + 1].copy()
+    V = state.V[:, :k].copy()
+    D = (1.0 - sigma[k] / sigma[:k]) / sigma[:k]
+    beta = beta_closed_form(sigma, V)
+    lam = sigma[k] / state.s
+    m_star = beta / lam
+    m = int(min(state.n, max(1, np.floor(m_star))))
+    return OracleState(state.X, state.kernel, state.bandwidth, state.r, state.Xs, sigma, V, D,
+                       float(beta), float(lam), float(m_star), m)
+
+
+def choose_rank(state, m_G):
+    """Eq. 7 with q = k+1: the largest k <= state.k with m*(k) <= m_G (0 if
+    none)."""
+    best = 0
+    for k in range(state.k + 1):
+        if with_rank(state, k).m_star <= m_G:
+            best = k
+    return best
+
+
+def acceleration(state_k, m_G):
+    """beta(K) / beta(K_G) * m_G / m*(k): beta(K) = 1 for the normalised
+    kernels and m*(k) = s / sigma_1 for the original kernel."""
+    return (1.0 / state_k.beta) * m_G / (state_k.s / state_k.sigma[0])

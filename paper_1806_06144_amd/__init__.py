@@ -30,7 +30,8 @@ class EpInfo(ctypes.Structure):
                 ("sigma_1", ctypes.c_double), ("sigma_k1", ctypes.c_double),
                 ("lambda_k1", ctypes.c_double), ("beta", ctypes.c_double),
                 ("m_star", ctypes.c_double), ("m", ctypes.c_int64),
-                ("eta", ctypes.c_double), ("setup_ms", ctypes.c_double)]
+                ("eta", ctypes.c_double), ("setup_ms", ctypes.c_double),
+                ("k_max", ctypes.c_int64), ("accel", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -69,6 +70,11 @@ def _load():
         "ep_get_preconditioner": (I, [P, P, P, P, P]),
         "ep_get_info": (I, [P, ctypes.POINTER(EpInfo)]),
         "ep_set_checks": (I, [P, I]),
+        "ep_set_rank": (I, [P, I64]),
+        "ep_adapt": (I, [P, I64, ctypes.POINTER(EpInfo)]),
+        "ep_batch_sweep": (I, [P, P, I, I, P]),
+        "ep_resource_batch": (I, [P, ctypes.c_double, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                  ctypes.POINTER(I64)]),
         "ep_timing_enable": (I, [P, I]),
         "ep_timing_read": (I, [P, ctypes.POINTER(EpTiming)]),
         "ep_sync": (I, [P]),
@@ -214,6 +220,32 @@ def ep_get_info(ctx):
     info = EpInfo()
     _check(_lib.ep_get_info(ctx, ctypes.byref(info)))
     return info
+
+
+def ep_set_rank(ctx, k):
+    return _check(_lib.ep_set_rank(ctx, k))
+
+
+def ep_adapt(ctx, m_G):
+    info = EpInfo()
+    _check(_lib.ep_adapt(ctx, m_G, ctypes.byref(info)))
+    return info
+
+
+def ep_batch_sweep(ctx, ms, reps=3):
+    """ms per fused step-2 pass for each batch size in ms."""
+    import numpy as np
+    arr = np.ascontiguousarray(np.asarray(ms, dtype=np.int64))
+    out = np.zeros(arr.shape[0], dtype=np.float64)
+    _check(_lib.ep_batch_sweep(ctx, arr.ctypes.data, arr.shape[0], reps, out.ctypes.data))
+    return out
+
+
+def ep_resource_batch(ctx, tol=0.1):
+    """(m_C, m_S, m_G) of Section 3 Step 1."""
+    mc, ms, mg = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.ep_resource_batch(ctx, tol, ctypes.byref(mc), ctypes.byref(ms), ctypes.byref(mg)))
+    return mc.value, ms.value, mg.value
 
 
 def ep_set_checks(ctx, on):

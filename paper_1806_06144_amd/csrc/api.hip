@@ -86,12 +86,14 @@ struct ep_ctx {
     hipStream_t stream = nullptr;
     const float* X = nullptr;
     int64_t n = 0, d = 0, l = 0, s = 0, k = 0;
+    int64_t k_max = 0;                  // rank of the eigensystem held; k <= k_max is applied
     int kind = 0;
     float bandwidth = 1.f;
     float scale = 0.f;
     int64_t l_pad = 0, n_pad = 0, s_pad = 0, k_ld = 1;
     ep_info info{};
-    std::vector<double> sigma, D;
+    std::vector<double> sigma, D;       // sigma: k_max+1 values; D: k values
+    std::vector<float> Vh;              // host copy of V (s x k_max)
     std::vector<int64_t> r_host;
     bool checks = false;
     std::vector<unsigned char> seen;
@@ -280,6 +282,79 @@ int eigensystem_from_saved(ep_ctx* c, const double* sigma, const float* V,
     return EP_OK;
 }
 
+// beta(K_G) for every rank k' <= k_max at once (Section 3 Step 2 with the
+// Nystrom eigenfunctions of Section 4, over the subsample points):
+//   beta(k') = max_i [1 - sum_{j<k'} (sigma_j - sigma_k') V_ij^2]
+//            = max_i [1 - A_i(k') + sigma_k' B_i(k')],
+// A_i, B_i prefix sums of sigma_j V_ij^2 and V_ij^2.
+std::vector<double> beta_all_ranks(const ep_ctx* c) {
+    const int64_t s = c->s, km = c->k_max;
+    std::vector<double> beta(km + 1, -1e300), A(s, 0.0), B(s, 0.0);
+    for (int64_t kk = 0; kk <= km; ++kk) {
+        const double floor_sigma = c->sigma[kk];
+        double best = -1e300;
+        for (int64_t i = 0; i < s; ++i) best = std::max(best, 1.0 - A[i] + floor_sigma * B[i]);
+        beta[kk] = kk == 0 ? 1.0 : best;
+        if (kk < km) {
+            for (int64_t i = 0; i < s; ++i) {
+                const double v = c->Vh[(size_t)i * km + kk];
+                A[i] += c->sigma[kk] * v * v;
+                B[i] += v * v;
+            }
+        }
+    }
+    return beta;
+}
+
+// Make rank k (0 <= k <= k_max) the active preconditioner: D (Section 4,
+// Eq. 8 with q = k+1), beta(K_G), lambda = sigma_{k+1}/s, m* = beta/lambda
+// (Section 2), batch min(n, max(1, floor(m*))) and its step size.
+int apply_rank(ep_ctx* c, int64_t k) {
+    const int64_t s = c->s, n = c->n;
+    c->k = k;
+    c->D.resize(k);
+    std::vector<float> dk(std::max<int64_t>(c->k_max, 1), 0.f);
+    for (int64_t i = 0; i < k; ++i) {
+        c->D[i] = (1.0 - c->sigma[k] / c->sigma[i]) / c->sigma[i];
+        dk[i] = (float)c->D[i];
+    }
+    HIP_TRY(hipMemcpyAsync(c->Dk.p, dk.data(), dk.size() * sizeof(float), hipMemcpyHostToDevice,
+                           c->stream));
+    double beta = 1.0;
+    if (k > 0) {
+        beta = -1e300;
+        const int64_t km = c->k_max;
+        for (int64_t i = 0; i < s; ++i) {
+            double acc = 0.0;
+            for (int64_t j = 0; j < k; ++j) {
+                const double v = c->Vh[(size_t)i * km + j];
+                acc += (c->sigma[j] - c->sigma[k]) * v * v;
+            }
+            beta = std::max(beta, 1.0 - acc);
+        }
+    }
+    const double lam = c->sigma[k] / (double)s;
+    const double m_star = beta / lam;
+    const int64_t m = std::min<int64_t>(n, std::max<int64_t>(1, (int64_t)std::floor(m_star)));
+    ep_info& I = c->info;
+    I.n = n;
+    I.d = c->d;
+    I.l = c->l;
+    I.s = s;
+    I.k = k;
+    I.k_max = c->k_max;
+    I.sigma_1 = c->sigma[0];
+    I.sigma_k1 = c->sigma[k];
+    I.lambda_k1 = lam;
+    I.beta = beta;
+    I.m_star = m_star;
+    I.m = m;
+    I.eta = (double)m / (beta + (double)(m - 1) * lam);
+    I.accel = 0.0;
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    return EP_OK;
+}
+
 int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sigma_in,
              const float* V_in) {
     std::vector<double> kpd;
@@ -338,42 +413,17 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sig
                       : eigensystem_from_solver(c, kpd);
     if (rc) return rc;
 
-    // D_i = (1 - sigma_{k+1}/sigma_i) / sigma_i (Section 4, Eq. 8 with q = k+1)
-    c->D.resize(k);
-    std::vector<float> dk(c->k_ld, 0.f);
-    for (int64_t i = 0; i < k; ++i) {
-        c->D[i] = (1.0 - c->sigma[k] / c->sigma[i]) / c->sigma[i];
-        dk[i] = (float)c->D[i];
-    }
-    HIP_TRY(hipMemcpyAsync(c->Dk.p, dk.data(), c->k_ld * sizeof(float), hipMemcpyHostToDevice, st));
     int herr = 0;
     HIP_TRY(hipMemcpyAsync(&herr, c->err.p, sizeof(int), hipMemcpyDeviceToHost, st));
+    c->Vh.resize((size_t)s * k);
+    if (k > 0)
+        HIP_TRY(hipMemcpyAsync(c->Vh.data(), c->V.p, (size_t)s * k * sizeof(float),
+                               hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
     if (herr) return fail(EP_EINVAL, "subsample index out of range");
-
-    // Section 3 Step 2: beta(K_G) over the subsample points; lambda_1(K_G) =
-    // sigma_{k+1}/s; Section 2: m* = beta / lambda_1; Step 3: batch and step.
-    double beta = -1e300;
-    for (double v : kpd) beta = std::max(beta, v);
-    if (k == 0) beta = 1.0;
-    const double lam = c->sigma[k] / (double)s;
-    const double m_star = beta / lam;
-    const int64_t m = std::min<int64_t>(n, std::max<int64_t>(1, (int64_t)std::floor(m_star)));
-
-    ep_info& I = c->info;
-    I.n = n;
-    I.d = d;
-    I.l = c->l;
-    I.s = s;
-    I.k = k;
-    I.sigma_1 = c->sigma[0];
-    I.sigma_k1 = c->sigma[k];
-    I.lambda_k1 = lam;
-    I.beta = beta;
-    I.m_star = m_star;
-    I.m = m;
-    I.eta = (double)m / (beta + (double)(m - 1) * lam);
-    return EP_OK;
+    (void)kpd;
+    c->k_max = k;
+    return apply_rank(c, k);
 }
 
 int ensure_step_buffers(ep_ctx* c, int64_t m) {
@@ -585,10 +635,115 @@ int ep_get_preconditioner(ep_ctx* c, double* sigma, double* D, float* V, int64_t
     if (D && c->k) std::memcpy(D, c->D.data(), c->k * sizeof(double));
     if (r) std::memcpy(r, c->r_host.data(), c->s * sizeof(int64_t));
     if (V && c->k) {
-        HIP_TRY(hipMemcpyAsync(V, c->V.p, (size_t)c->s * c->k * sizeof(float),
-                               hipMemcpyDeviceToHost, c->stream));
-        HIP_TRY(hipStreamSynchronize(c->stream));
+        // active rank k of the held V (row stride k_max)
+        for (int64_t i = 0; i < c->s; ++i)
+            std::memcpy(V + i * c->k, c->Vh.data() + (size_t)i * c->k_max, c->k * sizeof(float));
     }
+    return EP_OK;
+}
+
+int ep_set_rank(ep_ctx* c, int64_t k) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (k < 0 || k > c->k_max)
+        return fail(EP_EINVAL, "rank %lld outside [0, %lld]", (long long)k, (long long)c->k_max);
+    DeviceGuard dg(c->device);
+    return apply_rank(c, k);
+}
+
+int ep_adapt(ep_ctx* c, int64_t m_G, ep_info* info) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (m_G < 1) return fail(EP_EINVAL, "m_G must be >= 1");
+    DeviceGuard dg(c->device);
+    // Section 3 Step 2, Eq. 7: the largest rank whose adapted kernel has a
+    // critical batch m*(k) = beta(k) s / sigma_{k+1} no larger than m_G
+    const std::vector<double> beta = beta_all_ranks(c);
+    int64_t best = 0;
+    for (int64_t kk = 0; kk <= c->k_max; ++kk) {
+        const double mstar = beta[kk] * (double)c->s / c->sigma[kk];
+        if (mstar <= (double)m_G) best = kk;
+    }
+    int rc = apply_rank(c, best);
+    if (rc) return rc;
+    // Section 3 Step 3: batch m = m_G with the step size for that batch
+    ep_info& I = c->info;
+    I.m = std::min<int64_t>(c->n, m_G);
+    I.eta = (double)I.m / (I.beta + (double)(I.m - 1) * I.lambda_k1);
+    // Section 3 Claim: acceleration beta(K)/beta(K_G) * m_G / m*(k), with
+    // beta(K) = 1 and m*(k) = s / sigma_1 for the original kernel
+    I.accel = (1.0 / I.beta) * (double)I.m / ((double)c->s / c->sigma[0]);
+    if (info) *info = I;
+    return EP_OK;
+}
+
+int ep_batch_sweep(ep_ctx* c, const int64_t* ms, int count, int reps, double* ms_per_pass) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (!ms || !ms_per_pass || count < 0 || reps < 1) return fail(EP_EINVAL, "bad arguments");
+    for (int i = 0; i < count; ++i)
+        if (ms[i] < 1 || ms[i] > c->n) return fail(EP_EINVAL, "batch size outside [1, n]");
+    DeviceGuard dg(c->device);
+    hipEvent_t e0, e1;
+    HIP_TRY(hipEventCreate(&e0));
+    HIP_TRY(hipEventCreate(&e1));
+    int rc = EP_OK;
+    for (int i = 0; i < count && rc == EP_OK; ++i) {
+        const int64_t m = ms[i];
+        int slices = 0;
+        int64_t rows_pad = 0;
+        // the step-2 pass with the first m rows of X as the batch
+        rc = run_kmv(c, c->X, c->d, c->norms.as<float>(), nullptr, m, c->X, c->d,
+                     c->norms.as<float>(), nullptr, c->n, c->alpha.as<float>(), &slices, &rows_pad,
+                     false, false);
+        if (rc) break;
+        if (hipEventRecord(e0, c->stream) != hipSuccess) rc = fail(EP_EDEVICE, "event record");
+        for (int r = 0; r < reps && rc == EP_OK; ++r)
+            rc = run_kmv(c, c->X, c->d, c->norms.as<float>(), nullptr, m, c->X, c->d,
+                         c->norms.as<float>(), nullptr, c->n, c->alpha.as<float>(), &slices,
+                         &rows_pad, false, false);
+        float t = 0.f;
+        if (rc == EP_OK && (hipEventRecord(e1, c->stream) != hipSuccess ||
+                            hipEventSynchronize(e1) != hipSuccess ||
+                            hipEventElapsedTime(&t, e0, e1) != hipSuccess))
+            rc = fail(EP_EDEVICE, "event timing failed");
+        ms_per_pass[i] = t / reps;
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    return rc;
+}
+
+int ep_resource_batch(ep_ctx* c, double tol, int64_t* m_C, int64_t* m_S, int64_t* m_G) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (!(tol > 0.0 && tol < 1.0)) return fail(EP_EINVAL, "tol must be in (0, 1)");
+    DeviceGuard dg(c->device);
+    // Section 3 Step 1. m_S: batch at which the paper's memory model
+    // (d + l + m) n floats fills the device; m_C: the smallest batch whose
+    // kernel-entry throughput is within tol of the best measured, i.e. where
+    // time per step stops being flat.
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, c->device));
+    const double floats = (double)prop.totalGlobalMem / 4.0;
+    const int64_t ms_cap = (int64_t)(floats / (double)c->n) - c->d - c->l;
+    std::vector<int64_t> grid;
+    for (int64_t m = 32; m <= std::min<int64_t>(c->n, 32768); m *= 2) grid.push_back(m);
+    if (grid.empty()) grid.push_back(c->n);
+    std::vector<double> t(grid.size());
+    int rc = ep_batch_sweep(c, grid.data(), (int)grid.size(), 2, t.data());
+    if (rc) return rc;
+    double best = 0.0;
+    for (size_t i = 0; i < grid.size(); ++i) best = std::max(best, (double)grid[i] / t[i]);
+    int64_t mc = grid.back();
+    for (size_t i = 0; i < grid.size(); ++i)
+        if ((double)grid[i] / t[i] >= (1.0 - tol) * best) {
+            mc = grid[i];
+            break;
+        }
+    if (m_C) *m_C = mc;
+    if (m_S) *m_S = std::max<int64_t>(1, ms_cap);
+    if (m_G) *m_G = std::max<int64_t>(1, std::min(mc, ms_cap));
     return EP_OK;
 }
 
