@@ -89,6 +89,128 @@ def cpu_baseline(X, alpha_host, cfg, target_s=15.0):
     }
 
 
+def study_batch(args):
+    """Synthetic analogue of the paper's batch-size / GPU-utilisation study
+    (Section 5, Figure 4): time per step against batch size on a
+    TIMIT-shaped problem (n = 1e5, d = 440, l = 144), the resource batch of
+    Section 3 Step 1, the Eq. 7 rank for it, and time per epoch against n at
+    that batch."""
+    import torch
+    import synth
+    import paper_1806_06144_amd as ep
+    dev = torch.device("cuda:0")
+    base = synth.get_config("timit")
+    out = []
+    cfg = synth.get_config("timit", n=100000, s=4000, k=400)
+    X = synth.features(cfg, 0)
+    Xd = torch.from_numpy(X).to(dev)
+    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
+                            sub_idx=synth.subsample_indices(cfg, 0))
+    ms = [2 ** j for j in range(4, 15)]
+    t = ep.ep_batch_sweep(ctx, ms, reps=3)
+    for m, tm in zip(ms, t):
+        rec = {"study": "time_per_step_vs_batch", "n": cfg.n, "d": cfg.d, "l": cfg.l, "m": m,
+               "fused_pass_ms": tm, "entries_per_s": m * cfg.n / (tm * 1e-3)}
+        out.append(rec)
+        log(json.dumps(rec))
+    m_C, m_S, m_G = ep.ep_resource_batch(ctx, 0.1)
+    info0 = ep.ep_adapt(ctx, 1)                   # rank of the original kernel's m*
+    ep.ep_set_rank(ctx, 0)
+    mstar0 = ep.ep_get_info(ctx).m_star
+    ad = ep.ep_adapt(ctx, m_G)
+    rec = {"study": "resource_adaptive", "n": cfg.n, "k_max": cfg.k, "m_C": m_C, "m_S": m_S,
+           "m_G": m_G, "chosen_k": ad.k, "m_star_original": mstar0, "m_star_adapted": ad.m_star,
+           "beta_adapted": ad.beta, "sigma_1": ad.sigma_1, "sigma_k1": ad.sigma_k1,
+           "acceleration": ad.accel, "step_eta": ad.eta}
+    del info0
+    out.append(rec)
+    log(json.dumps(rec))
+    ep.ep_destroy(ctx)
+    del Xd
+    torch.cuda.empty_cache()
+    # time per epoch against n at the adapted batch and rank
+    for n in [25000, 100000, 400000, base.n]:
+        c = synth.get_config("timit", n=n, s=4000, k=ad.k)
+        Xn = synth.features(c, 0)
+        labels = synth.class_labels(c, Xn, 0)
+        Xd = torch.from_numpy(Xn).to(dev)
+        ctx, inf = ep.ep_setup(Xd, c.n, c.d, c.l, c.kernel, c.bandwidth, c.s, c.k,
+                               sub_idx=synth.subsample_indices(c, 0))
+        m = min(n, m_G)
+        batches = synth.epoch_batches(n, m, 0)
+        tl = [torch.from_numpy(b).to(dev) for b in batches]
+        yl = [torch.from_numpy(synth.one_hot(labels[b], c.l)).to(dev) for b in batches]
+        ep.ep_step(ctx, tl[0], len(batches[0]), yl[0])
+        ep.ep_sync(ctx)
+        t0 = time.perf_counter()
+        for tb, yb, b in zip(tl, yl, batches):
+            ep.ep_step(ctx, tb, len(b), yb)
+        ep.ep_sync(ctx)
+        dt = time.perf_counter() - t0
+        rec = {"study": "time_per_epoch_vs_n", "n": n, "m": m, "k": c.k, "steps": len(batches),
+               "epoch_s": dt}
+        out.append(rec)
+        log(json.dumps(rec))
+        ep.ep_destroy(ctx)
+        del Xd, tl, yl
+        torch.cuda.empty_cache()
+    return out
+
+
+def study_convergence(args):
+    """Synthetic analogue of the paper's convergence comparison (Section 5,
+    Figure 3): epochs and GPU time to bring the training MSE (mean over
+    points and labels) below a threshold, against batch size, for plain
+    kernel SGD (rank 0, its own optimal step) and EigenPro 2.0 (the Eq. 7
+    rank for the resource batch), on a TIMIT-shaped problem with n = 1e5."""
+    import torch
+    import synth
+    import paper_1806_06144_amd as ep
+    dev = torch.device("cuda:0")
+    cfg = synth.get_config("timit", n=100000, s=4000, k=400)
+    X = synth.features(cfg, 0)
+    labels = synth.class_labels(cfg, X, 0)
+    Xd = torch.from_numpy(X).to(dev)
+    Y = torch.from_numpy(synth.one_hot(labels, cfg.l)).to(dev)
+    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
+                            sub_idx=synth.subsample_indices(cfg, 0))
+    _, _, m_G = ep.ep_resource_batch(ctx, 0.1)
+    k_ad = ep.ep_adapt(ctx, m_G).k
+    P = torch.empty_like(Y)
+    thr, max_epochs, budget_s = 2e-4, 40, 60.0
+    out = []
+
+    def mse():
+        ep.ep_predict(ctx, Xd, cfg.n, P)
+        ep.ep_sync(ctx)
+        return float(((P - Y) ** 2).mean())
+
+    for k in (0, k_ad):
+        ep.ep_set_rank(ctx, k)
+        for m in (64, 256, 1024, 4096):
+            ep.ep_set_alpha(ctx, torch.zeros_like(Y))
+            gpu_s, epochs, err = 0.0, 0, mse()
+            while err >= thr and epochs < max_epochs and gpu_s < budget_s:
+                batches = synth.epoch_batches(cfg.n, m, epochs)
+                tl = [torch.from_numpy(b).to(dev) for b in batches]
+                yl = [Y[b] for b in tl]
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for tb, yb in zip(tl, yl):
+                    ep.ep_step(ctx, tb, tb.shape[0], yb)
+                ep.ep_sync(ctx)
+                gpu_s += time.perf_counter() - t0
+                epochs += 1
+                err = mse()
+            rec = {"study": "convergence", "n": cfg.n, "k": k, "m": m, "epochs": epochs,
+                   "step_time_s": gpu_s, "train_mse": err, "threshold": thr,
+                   "converged": err < thr}
+            out.append(rec)
+            log(json.dumps(rec))
+    ep.ep_destroy(ctx)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,7 +229,14 @@ def main():
                     help="rebuild the context from a saved setup (ep_restore; no eigensolve)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--study", choices=["batch", "convergence"], default=None,
+                    help="run a study instead of the benchmark (JSON lines on stdout)")
     args = ap.parse_args()
+    if args.study:
+        fn = {"batch": study_batch, "convergence": study_convergence}[args.study]
+        for rec in fn(args):
+            print(json.dumps(rec), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "this build has no multi-GPU path.", file=sys.stderr)
