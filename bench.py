@@ -66,18 +66,26 @@ def cpu_baseline(X, alpha_host, cfg, target_s=15.0):
         cores = os.cpu_count() or 1
     rng = np.random.default_rng(123)
     kid = {"gaussian": oracle.GAUSSIAN, "laplacian": oracle.LAPLACIAN}[cfg.kernel]
-    rows = 8
-    t0 = time.perf_counter()
-    oracle.predict(X, alpha_host, X[rng.choice(X.shape[0], rows, replace=False)], kid,
-                   cfg.bandwidth)
-    dt = time.perf_counter() - t0
-    rows2 = int(max(rows, min(X.shape[0], 20000, rows * target_s / max(dt, 1e-3))))
-    if rows2 > rows * 1.5:
+    def timed(rows):
+        Q = X[rng.choice(X.shape[0], rows, replace=False)]
         t0 = time.perf_counter()
-        oracle.predict(X, alpha_host, X[rng.choice(X.shape[0], rows2, replace=False)], kid,
-                       cfg.bandwidth)
-        dt = time.perf_counter() - t0
-        rows = rows2
+        oracle.predict(X, alpha_host, Q, kid, cfg.bandwidth)
+        return time.perf_counter() - t0
+
+    # Each call pays a per-centre cost (converting and norming X block by
+    # block) plus a per-row cost, so time grows more slowly than the row
+    # count; scaling the rows by target/time therefore stays below the
+    # target, and two rescales bring the reported call near it.
+    rows = 64
+    dt = timed(rows)
+    for _ in range(2):
+        if dt >= 0.5 * target_s:
+            break
+        grown = int(min(X.shape[0], 20000, rows * target_s / max(dt, 1e-3)))
+        if grown <= rows:
+            break
+        rows = grown
+        dt = timed(rows)
     return {
         "value": rows * X.shape[0] / dt,
         "unit": "entries/s",
@@ -211,6 +219,48 @@ def study_convergence(args):
     return out
 
 
+def study_setup(args):
+    """Setup eigensolve at the subsample size and rank of each workload:
+    the full divide-and-conquer eigendecomposition against the
+    Chebyshev-filtered subspace iteration (both float64 on the device), on
+    s rows drawn from the workload's law (taken as the subsample), with the
+    largest eigenvalue difference and the V D V^T difference between them."""
+    import torch
+    import synth
+    import paper_1806_06144_amd as ep
+    dev = torch.device("cuda:0")
+    out = []
+    for name in ["mnist", "cifar", "timit", "imagenet"]:
+        base = synth.get_config(name)
+        cfg = synth.get_config(name, n=base.s)
+        X = synth.features(cfg, 0)
+        Xd = torch.from_numpy(X).to(dev)
+        r = np.arange(cfg.s, dtype=np.int64)
+        res = {}
+        for solver in ["dense", "subspace", "dense", "subspace"]:    # second pass timed warm
+            ctx, info = ep.ep_setup_ex(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth,
+                                       cfg.s, cfg.k, sub_idx=r,
+                                       opts={"solver": solver, "no_fallback": 1})
+            sigma, D, V, _ = ep.ep_get_preconditioner(ctx, info)
+            ep.ep_destroy(ctx)
+            res[solver] = (info, sigma, (V.astype(np.float64) * D) @ V.T.astype(np.float64))
+        (i_d, s_d, L_d), (i_s, s_s, L_s) = res["dense"], res["subspace"]
+        rec = {"study": "setup_eigensolver", "workload": name, "s": cfg.s, "d": cfg.d,
+               "k": cfg.k, "kernel": cfg.kernel,
+               "dense_setup_ms": i_d.setup_ms, "subspace_setup_ms": i_s.setup_ms,
+               "speedup": i_d.setup_ms / i_s.setup_ms,
+               "subspace_iters": i_s.solver_iters, "subspace_matvecs": i_s.solver_matvecs,
+               "subspace_eig_residual": i_s.eig_residual,
+               "max_rel_sigma_diff": float(np.max(np.abs(s_s - s_d) / s_d)),
+               "lowrank_rel_diff": float(np.linalg.norm(L_s - L_d) / np.linalg.norm(L_d)),
+               "sigma_1": i_s.sigma_1, "sigma_k1": i_s.sigma_k1}
+        out.append(rec)
+        log(json.dumps(rec))
+        del Xd
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -229,11 +279,12 @@ def main():
                     help="rebuild the context from a saved setup (ep_restore; no eigensolve)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
-    ap.add_argument("--study", choices=["batch", "convergence"], default=None,
+    ap.add_argument("--study", choices=["batch", "convergence", "setup"], default=None,
                     help="run a study instead of the benchmark (JSON lines on stdout)")
     args = ap.parse_args()
     if args.study:
-        fn = {"batch": study_batch, "convergence": study_convergence}[args.study]
+        fn = {"batch": study_batch, "convergence": study_convergence,
+              "setup": study_setup}[args.study]
         for rec in fn(args):
             print(json.dumps(rec), flush=True)
         return

@@ -63,7 +63,41 @@ typedef struct ep_info {
                            ep_adapt)                                         */
     double accel;       /* after ep_adapt: beta(K)/beta(K_G) * m_G / m*(k),
                            the acceleration of Section 3's claim (0 before)  */
+    int64_t solver;     /* eigensolver that produced sigma and V:
+                           EP_SOLVER_DENSE or EP_SOLVER_SUBSPACE; 0 after
+                           ep_restore (none ran)                              */
+    int64_t solver_iters;   /* SUBSPACE: outer (filter + Rayleigh-Ritz)
+                               iterations; 0 otherwise                        */
+    int64_t solver_matvecs; /* SUBSPACE: products of K_s with a vector, in
+                               total; 0 otherwise                             */
+    double eig_residual;    /* SUBSPACE: max_j |K_s v_j - sigma_j v_j| /
+                               sigma_1 over the k+1 pairs; 0 otherwise        */
 } ep_info;
+
+/* Eigensolvers for the top k+1 eigenpairs of K_s (ep_setup_opts.solver). */
+enum {
+    EP_SOLVER_AUTO = 0,     /* SUBSPACE when s >= 2048 and the block
+                               (k+1+guard columns) is at most s/16; else
+                               DENSE                                          */
+    EP_SOLVER_DENSE = 1,    /* full divide-and-conquer eigendecomposition of
+                               K_s (rocSOLVER dsyevd), O(s^3)                 */
+    EP_SOLVER_SUBSPACE = 2  /* Chebyshev-filtered block subspace iteration with
+                               Rayleigh-Ritz and locking, O(s^2 (k+guard))
+                               per filter degree                              */
+};
+
+/* Options of ep_setup_ex; zero in any field selects its default. */
+typedef struct ep_setup_opts {
+    int32_t solver;      /* EP_SOLVER_*                         (AUTO)        */
+    int32_t max_degree;  /* cap on the Chebyshev degree of one filter (20)    */
+    int32_t max_iters;   /* outer iterations before giving up      (100)      */
+    int32_t no_fallback; /* nonzero: a SUBSPACE solve that does not converge
+                            returns EP_ENUMERIC; zero: DENSE runs instead     */
+    int64_t guard;       /* block columns beyond k+1: max(32, (k+1)/4)
+                            rounded up to a multiple of 16                    */
+    double tol;          /* a Ritz pair is accepted when |K_s v - theta v| <=
+                            tol * sigma_1                           (1e-11)   */
+} ep_setup_opts;
 
 /*
  * ep_setup — Algorithm 1 initialisation, Section 4 (Nystrom extension) and
@@ -83,7 +117,8 @@ typedef struct ep_info {
  *   hip_stream hipStream_t to enqueue all work on (NULL = default stream).
  *   info       out (may be NULL): see ep_info.
  * Sets alpha = 0. Blocks until setup is complete. K_s is formed in float64;
- * the eigensolve runs on the device in float64.
+ * the eigensolve runs on the device in float64 with EP_SOLVER_AUTO (see
+ * ep_setup_ex).
  * Errors: EP_EINVAL (ranges above, duplicate/out-of-range sub_idx),
  * EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC.
  */
@@ -91,6 +126,24 @@ int ep_setup(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
              int kernel, float bandwidth, int64_t s, int64_t k,
              const int64_t* sub_idx, uint64_t seed, void* hip_stream,
              ep_info* info);
+
+/*
+ * ep_setup_ex — ep_setup with a choice of eigensolver for K_s (Algorithm 1
+ * initialisation; the Nystrom extension of Section 4 needs sigma_1 ..
+ * sigma_{k+1} and v_1 .. v_k only, so the full spectrum need not be formed).
+ *   opts  host, may be NULL (all defaults; then identical to ep_setup).
+ * Both solvers work in float64 on K_s. SUBSPACE starts from a block drawn
+ * from `seed` and accepts a pair at the residual bound opts->tol; its
+ * eigenvalues agree with DENSE to that bound or better, and V D V^T (the
+ * only use of the eigenvectors) is insensitive to rotations within
+ * clusters of nearly equal eigenvalues. Errors: as ep_setup, plus
+ * EP_EINVAL for an unknown solver or negative option, and EP_ENUMERIC when
+ * SUBSPACE does not converge and no_fallback is set.
+ */
+int ep_setup_ex(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
+                int kernel, float bandwidth, int64_t s, int64_t k,
+                const int64_t* sub_idx, uint64_t seed, void* hip_stream,
+                const ep_setup_opts* opts, ep_info* info);
 
 /*
  * ep_restore — rebuild a context from a saved setup (checkpoint / resume):

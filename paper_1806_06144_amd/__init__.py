@@ -19,6 +19,8 @@ HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "eigenpro.h")
 
 EP_OK, EP_EINVAL, EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC, EP_EINDEX = 0, -1, -2, -3, -4, -5
 EP_GAUSSIAN, EP_LAPLACIAN = 0, 1
+EP_SOLVER_AUTO, EP_SOLVER_DENSE, EP_SOLVER_SUBSPACE = 0, 1, 2
+SOLVERS = {"auto": EP_SOLVER_AUTO, "dense": EP_SOLVER_DENSE, "subspace": EP_SOLVER_SUBSPACE}
 KERNELS = {"gaussian": EP_GAUSSIAN, "laplacian": EP_LAPLACIAN}
 _CODES = {EP_EINVAL: "EP_EINVAL", EP_ENOMEM: "EP_ENOMEM", EP_EDEVICE: "EP_EDEVICE",
           EP_ENUMERIC: "EP_ENUMERIC", EP_EINDEX: "EP_EINDEX"}
@@ -31,10 +33,18 @@ class EpInfo(ctypes.Structure):
                 ("lambda_k1", ctypes.c_double), ("beta", ctypes.c_double),
                 ("m_star", ctypes.c_double), ("m", ctypes.c_int64),
                 ("eta", ctypes.c_double), ("setup_ms", ctypes.c_double),
-                ("k_max", ctypes.c_int64), ("accel", ctypes.c_double)]
+                ("k_max", ctypes.c_int64), ("accel", ctypes.c_double),
+                ("solver", ctypes.c_int64), ("solver_iters", ctypes.c_int64),
+                ("solver_matvecs", ctypes.c_int64), ("eig_residual", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class EpSetupOpts(ctypes.Structure):
+    _fields_ = [("solver", ctypes.c_int32), ("max_degree", ctypes.c_int32),
+                ("max_iters", ctypes.c_int32), ("no_fallback", ctypes.c_int32),
+                ("guard", ctypes.c_int64), ("tol", ctypes.c_double)]
 
 
 class EpTiming(ctypes.Structure):
@@ -61,6 +71,9 @@ def _load():
     sig = {
         "ep_setup": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P,
                          ctypes.c_uint64, P, ctypes.POINTER(EpInfo)]),
+        "ep_setup_ex": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P,
+                            ctypes.c_uint64, P, ctypes.POINTER(EpSetupOpts),
+                            ctypes.POINTER(EpInfo)]),
         "ep_restore": (I, [ctypes.POINTER(P), P, I64, I64, I64, I, F, I64, I64, P, P, P, P,
                            ctypes.POINTER(EpInfo)]),
         "ep_step": (I, [P, P, I64, P, P]),
@@ -144,6 +157,13 @@ def ep_setup(X, n, d, l, kernel, bandwidth, s, k, sub_idx=None, seed=0, stream=N
     """Returns (ctx, EpInfo). X: device float32 n x d (borrowed: keep it
     alive until ep_destroy). sub_idx: host int64 sequence of s indices or
     None."""
+    return ep_setup_ex(X, n, d, l, kernel, bandwidth, s, k, sub_idx, seed, stream, None)
+
+
+def ep_setup_ex(X, n, d, l, kernel, bandwidth, s, k, sub_idx=None, seed=0, stream=None,
+                opts=None):
+    """ep_setup with setup options: ``opts`` is an EpSetupOpts, a dict of its
+    fields (``solver`` may be "auto", "dense" or "subspace"), or None."""
     torch = _torch()
     if isinstance(kernel, str):
         kernel = KERNELS[kernel]
@@ -156,10 +176,20 @@ def ep_setup(X, n, d, l, kernel, bandwidth, s, k, sub_idx=None, seed=0, stream=N
         if keep.shape != (s,):
             raise ValueError("sub_idx must hold s indices")
         sub_ptr = keep.ctypes.data
+    if isinstance(opts, dict):
+        o = dict(opts)
+        if isinstance(o.get("solver"), str):
+            o["solver"] = SOLVERS[o["solver"]]
+        opts = EpSetupOpts(**o)
     ctx = ctypes.c_void_p()
     info = EpInfo()
-    _check(_lib.ep_setup(ctypes.byref(ctx), xp, n, d, l, kernel, bandwidth, s, k, sub_ptr,
-                         seed, _stream_handle(stream), ctypes.byref(info)))
+    if opts is None:
+        _check(_lib.ep_setup(ctypes.byref(ctx), xp, n, d, l, kernel, bandwidth, s, k, sub_ptr,
+                             seed, _stream_handle(stream), ctypes.byref(info)))
+    else:
+        _check(_lib.ep_setup_ex(ctypes.byref(ctx), xp, n, d, l, kernel, bandwidth, s, k,
+                                sub_ptr, seed, _stream_handle(stream), ctypes.byref(opts),
+                                ctypes.byref(info)))
     return ctx, info
 
 

@@ -1,6 +1,7 @@
 // C ABI of libeigenpro: context, argument checking, buffer management and the
 // launch sequence of one EigenPro 2.0 iteration (Algorithm 1) on one GPU.
 #include "eigenpro.h"
+#include "ep_host.h"
 #include "ep_internal.h"
 
 #include <rocblas/rocblas.h>
@@ -19,11 +20,10 @@
 using namespace ep;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
-int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int code, const char* fmt, ...) {
+int ep::fail(int code, const char* fmt, ...) {
     char buf[512];
     va_list ap;
     va_start(ap, fmt);
@@ -33,40 +33,7 @@ int fail(int code, const char* fmt, ...) {
     return code;
 }
 
-#define HIP_TRY(expr)                                                                  \
-    do {                                                                               \
-        hipError_t e_ = (expr);                                                        \
-        if (e_ != hipSuccess)                                                          \
-            return fail(e_ == hipErrorOutOfMemory ? EP_ENOMEM : EP_EDEVICE, "%s: %s (%s)", \
-                        #expr, hipGetErrorString(e_), __func__);                       \
-    } while (0)
-
-// Grow-only device buffer.
-struct DevBuf {
-    void* p = nullptr;
-    size_t bytes = 0;
-    hipError_t ensure(size_t want) {
-        if (want <= bytes) return hipSuccess;
-        if (p) {
-            hipError_t e = hipFree(p);
-            if (e != hipSuccess) return e;
-            p = nullptr;
-            bytes = 0;
-        }
-        hipError_t e = hipMalloc(&p, std::max<size_t>(want, 256));
-        if (e == hipSuccess) bytes = want;
-        return e;
-    }
-    void release() {
-        if (p) (void)hipFree(p);
-        p = nullptr;
-        bytes = 0;
-    }
-    template <class T>
-    T* as() const {
-        return static_cast<T*>(p);
-    }
-};
+namespace {
 
 struct TimedPair {
     hipEvent_t a, b;
@@ -95,6 +62,8 @@ struct ep_ctx {
     std::vector<double> sigma, D;       // sigma: k_max+1 values; D: k values
     std::vector<float> Vh;              // host copy of V (s x k_max)
     std::vector<int64_t> r_host;
+    ep_setup_opts opts{};               // eigensolver choice of ep_setup_ex
+    uint64_t seed = 0;
     bool checks = false;
     std::vector<unsigned char> seen;
 
@@ -196,57 +165,101 @@ struct DeviceGuard {
 };
 
 // Top k+1 eigenpairs of K_s = [k(x_ri, x_rj)] (Algorithm 1 initialisation):
-// K_s is formed in float64 and solved with the full divide-and-conquer
-// eigensolver (on this device much faster than the subset solvers; K_s is
-// small next to X). Fills c->sigma, c->V and the adapted kernel's diagonal
-// k_G(x_ri, x_ri) at the subsample points.
+// K_s is formed in float64 on the device and solved there in float64,
+// either by the full divide-and-conquer eigendecomposition or by the
+// Chebyshev-filtered subspace iteration of eigsolve.hip (Section 4 needs
+// only the top k+1 pairs). Fills c->sigma, c->V and the adapted kernel's
+// diagonal k_G(x_ri, x_ri) at the subsample points.
 int eigensystem_from_solver(ep_ctx* c, std::vector<double>& kpd) {
     const int64_t s = c->s, k = c->k, d = c->d;
     hipStream_t st = c->stream;
-    DevBuf Ks, W, E, kp, sig_dev, iinfo;
-    struct Free {
-        DevBuf* b[6];
-        ~Free() {
-            for (DevBuf* x : b) x->release();
-        }
-    } guard{{&Ks, &W, &E, &kp, &sig_dev, &iinfo}};
+    const ep_setup_opts& o = c->opts;
+    EigOpts eo;
+    eo.max_degree = o.max_degree;
+    eo.max_iters = o.max_iters;
+    eo.guard = o.guard;
+    eo.tol = o.tol;
+    int solver = o.solver;
+    if (solver == EP_SOLVER_AUTO) {
+        const int64_t q = k + 1;
+        const int64_t guard = o.guard > 0 ? o.guard : round_up(std::max<int64_t>(32, q / 4), 16);
+        // measured crossover: the dense solve's O(s^3) wins below s ~ 16 p
+        solver = (s >= 2048 && 16 * (q + guard) <= s) ? EP_SOLVER_SUBSPACE : EP_SOLVER_DENSE;
+    }
+    DevBuf Ks, W, E, kp, sig_dev, iinfo, Vq;
     HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
-    HIP_TRY(W.ensure((size_t)s * sizeof(double)));
-    HIP_TRY(E.ensure((size_t)s * sizeof(double)));
     HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
     HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
-    HIP_TRY(iinfo.ensure(sizeof(rocblas_int)));
     HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
                                         Ks.as<double>(), st));
 
     rocblas_handle h = nullptr;
     if (rocblas_create_handle(&h) != rocblas_status_success)
         return fail(EP_EDEVICE, "rocblas_create_handle failed");
+    struct HandleGuard {
+        rocblas_handle h;
+        ~HandleGuard() { rocblas_destroy_handle(h); }
+    } hguard{h};
     rocblas_set_stream(h, st);
-    rocblas_int* dinfo = iinfo.as<rocblas_int>();
-    // eigenvalues ascending in W, eigenvectors overwrite K_s (column-major)
-    const rocblas_status rs =
-        rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)s,
-                         Ks.as<double>(), (rocblas_int)s, W.as<double>(), E.as<double>(), dinfo);
-    rocblas_destroy_handle(h);
-    if (rs != rocblas_status_success)
-        return fail(EP_EDEVICE, "rocsolver_dsyevd returned status %d", (int)rs);
-    rocblas_int hinfo = 0;
-    std::vector<double> w_asc(k + 1);
-    HIP_TRY(hipMemcpyAsync(&hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipMemcpyAsync(w_asc.data(), W.as<double>() + (s - k - 1), (k + 1) * sizeof(double),
-                           hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipStreamSynchronize(st));
-    if (hinfo != 0) return fail(EP_ENUMERIC, "eigensolve failed: info=%d", (int)hinfo);
-    c->sigma.assign(w_asc.rbegin(), w_asc.rend());
+
+    const double* Z = nullptr;            // eigenvector columns, float64, leading dim s
+    int64_t col0 = 0, col_step = 1;
+    if (solver == EP_SOLVER_SUBSPACE) {
+        EigStats stats;
+        std::vector<double> theta;
+        const int rc = subspace_topq(Ks.as<double>(), s, k + 1, eo, c->seed ^ 0x5EEDE16ull, h, st,
+                                     theta, Vq, stats);
+        if (rc == EP_OK) {
+            c->sigma = theta;
+            Z = Vq.as<double>();
+            col0 = 0;
+            col_step = 1;
+            c->info.solver = EP_SOLVER_SUBSPACE;
+            c->info.solver_iters = stats.iters;
+            c->info.solver_matvecs = stats.matvecs;
+            c->info.eig_residual = stats.max_residual;
+        } else if (rc != EP_ENUMERIC || o.no_fallback) {
+            return rc;
+        } else {
+            (void)hipStreamSynchronize(st);
+            solver = EP_SOLVER_DENSE;     // did not converge: full solve instead
+        }
+    }
+    if (solver == EP_SOLVER_DENSE) {
+        HIP_TRY(W.ensure((size_t)s * sizeof(double)));
+        HIP_TRY(E.ensure((size_t)s * sizeof(double)));
+        HIP_TRY(iinfo.ensure(sizeof(rocblas_int)));
+        rocblas_int* dinfo = iinfo.as<rocblas_int>();
+        // eigenvalues ascending in W, eigenvectors overwrite K_s (column-major)
+        const rocblas_status rs =
+            rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)s,
+                             Ks.as<double>(), (rocblas_int)s, W.as<double>(), E.as<double>(),
+                             dinfo);
+        if (rs != rocblas_status_success)
+            return fail(EP_EDEVICE, "rocsolver_dsyevd returned status %d", (int)rs);
+        rocblas_int hinfo = 0;
+        std::vector<double> w_asc(k + 1);
+        HIP_TRY(hipMemcpyAsync(&hinfo, dinfo, sizeof hinfo, hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipMemcpyAsync(w_asc.data(), W.as<double>() + (s - k - 1),
+                               (k + 1) * sizeof(double), hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipStreamSynchronize(st));
+        if (hinfo != 0) return fail(EP_ENUMERIC, "eigensolve failed: info=%d", (int)hinfo);
+        c->sigma.assign(w_asc.rbegin(), w_asc.rend());
+        // top k+1 eigenvectors are the last k+1 columns, ascending
+        Z = Ks.as<double>() + (size_t)(s - k - 1) * s;
+        col0 = k;
+        col_step = -1;
+        c->info.solver = EP_SOLVER_DENSE;
+        c->info.solver_iters = 0;
+        c->info.solver_matvecs = 0;
+        c->info.eig_residual = 0.0;
+    }
     if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
         return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
-    // top k+1 eigenvectors are the last k+1 columns
-    const double* Z = Ks.as<double>() + (size_t)(s - k - 1) * s;
     HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
                            hipMemcpyHostToDevice, st));
-    HIP_TRY(launch_extract_eigvecs(Z, s, s, k, sig_dev.as<double>(), c->V.as<float>(), c->k_ld,
-                                   kp.as<double>(), st));
+    HIP_TRY(launch_extract_eigvecs(Z, s, col0, col_step, s, k, sig_dev.as<double>(),
+                                   c->V.as<float>(), c->k_ld, kp.as<double>(), st));
     kpd.resize(s);
     HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
@@ -446,7 +459,8 @@ namespace {
 
 int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
            float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
-           void* hip_stream, ep_info* info, const double* sigma, const float* V) {
+           void* hip_stream, ep_info* info, const double* sigma, const float* V,
+           const ep_setup_opts* opts) {
     g_err.clear();
     if (!out) return fail(EP_EINVAL, "ctx out-pointer is NULL");
     *out = nullptr;
@@ -459,6 +473,13 @@ int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int ke
         return fail(EP_EINVAL, "bandwidth must be positive and finite");
     if (s > 46340) return fail(EP_EINVAL, "s = %lld exceeds the eigensolver's 32-bit index range",
                                (long long)s);
+    if (opts) {
+        if (opts->solver < EP_SOLVER_AUTO || opts->solver > EP_SOLVER_SUBSPACE)
+            return fail(EP_EINVAL, "unknown solver %d", (int)opts->solver);
+        if (opts->max_degree < 0 || opts->max_iters < 0 || opts->guard < 0 ||
+            !(opts->tol >= 0.0) || !std::isfinite(opts->tol))
+            return fail(EP_EINVAL, "setup options must be zero (default) or positive");
+    }
     const auto t0 = std::chrono::steady_clock::now();
     ep_ctx* c = new (std::nothrow) ep_ctx();
     if (!c) return fail(EP_ENOMEM, "host allocation failed");
@@ -476,6 +497,8 @@ int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int ke
     c->kind = kernel;
     c->bandwidth = bandwidth;
     c->scale = kernel_scale(kernel, bandwidth);
+    if (opts) c->opts = *opts;
+    c->seed = seed;
     const int rc = do_setup(c, sub_idx, seed, sigma, V);
     if (rc != EP_OK) {
         (void)hipStreamSynchronize(c->stream);
@@ -497,7 +520,14 @@ int ep_setup(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int 
              float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
              void* hip_stream, ep_info* info) {
     return create(out, X, n, d, l, kernel, bandwidth, s, k, sub_idx, seed, hip_stream, info,
-                  nullptr, nullptr);
+                  nullptr, nullptr, nullptr);
+}
+
+int ep_setup_ex(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
+                float bandwidth, int64_t s, int64_t k, const int64_t* sub_idx, uint64_t seed,
+                void* hip_stream, const ep_setup_opts* opts, ep_info* info) {
+    return create(out, X, n, d, l, kernel, bandwidth, s, k, sub_idx, seed, hip_stream, info,
+                  nullptr, nullptr, opts);
 }
 
 int ep_restore(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int kernel,
@@ -507,7 +537,7 @@ int ep_restore(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, in
     if (!sub_idx) return fail(EP_EINVAL, "ep_restore needs the saved sub_idx");
     if (!sigma) return fail(EP_EINVAL, "ep_restore needs the saved sigma");
     return create(out, X, n, d, l, kernel, bandwidth, s, k, sub_idx, 0, hip_stream, info, sigma,
-                  V);
+                  V, nullptr);
 }
 
 int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_out) {

@@ -87,9 +87,11 @@ hipError_t launch_lowrank_update(const float* V, int64_t ldv, const float* W1, i
 hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d,
                                        int kind, double bandwidth, double* Ks,
                                        hipStream_t st);
-hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t s, int64_t k,
-                                  const double* sigma_desc_dev, float* V, int64_t ldv,
-                                  double* kp_diag, hipStream_t st);
+// V[i, j] = Z[i + (col0 + j col_step) ldz] (float32, row-major, ldv) for
+// j < k, zero for k <= j < ldv; kp_diag[i] = 1 - sum_j (sig_j - sig_k) V_ij^2.
+hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t col0, int64_t col_step,
+                                  int64_t s, int64_t k, const double* sigma_desc_dev, float* V,
+                                  int64_t ldv, double* kp_diag, hipStream_t st);
 hipError_t launch_fill_f32(float* p, int64_t count, float v, hipStream_t st);
 
 }  // namespace ep

@@ -230,6 +230,7 @@ __global__ void __launch_bounds__(256) subsample_kernel_f64(const float* Xs, int
 // kp_diag[i] = 1 - sum_{j<k} (sigma_j - sigma_k) Z[i, k-j]^2: the adapted
 // kernel k_G(x_ri, x_ri) at each subsample point.
 __global__ void __launch_bounds__(256) extract_eigvecs_kernel(const double* Z, int64_t ldz,
+                                                              int64_t col0, int64_t col_step,
                                                               int64_t s, int64_t k,
                                                               const double* sig, float* V,
                                                               int64_t ldv, double* kp_diag) {
@@ -237,7 +238,7 @@ __global__ void __launch_bounds__(256) extract_eigvecs_kernel(const double* Z, i
     if (i >= s) return;
     double acc = 0.0;
     for (int64_t j = 0; j < k; ++j) {
-        const double z = Z[i + (k - j) * ldz];
+        const double z = Z[i + (col0 + j * col_step) * ldz];
         V[i * ldv + j] = (float)z;
         acc += (sig[j] - sig[k]) * z * z;
     }
@@ -347,11 +348,11 @@ hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d, in
     return hipGetLastError();
 }
 
-hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t s, int64_t k,
-                                  const double* sigma_desc_dev, float* V, int64_t ldv,
-                                  double* kp_diag, hipStream_t st) {
-    hipLaunchKernelGGL(extract_eigvecs_kernel, dim3(blocks_for(s)), dim3(256), 0, st, Z, ldz, s,
-                       k, sigma_desc_dev, V, ldv, kp_diag);
+hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t col0, int64_t col_step,
+                                  int64_t s, int64_t k, const double* sigma_desc_dev, float* V,
+                                  int64_t ldv, double* kp_diag, hipStream_t st) {
+    hipLaunchKernelGGL(extract_eigvecs_kernel, dim3(blocks_for(s)), dim3(256), 0, st, Z, ldz,
+                       col0, col_step, s, k, sigma_desc_dev, V, ldv, kp_diag);
     return hipGetLastError();
 }
 

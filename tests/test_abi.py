@@ -53,3 +53,15 @@ def test_calls_on_null_context():
     assert ep.raw_call("ep_set_checks", None, 1) == ep.EP_EINVAL
     assert ep.raw_call("ep_timing_enable", None, 1) == ep.EP_EINVAL
     ep.raw_call("ep_destroy", None)
+
+
+@pytest.mark.parametrize("opts", [
+    dict(solver=3), dict(solver=-1), dict(max_degree=-1), dict(max_iters=-2),
+    dict(guard=-5), dict(tol=-1e-9), dict(tol=float("nan")), dict(tol=float("inf")),
+])
+def test_setup_ex_rejects_bad_options(opts):
+    o = ep.EpSetupOpts(**opts)
+    rc = ep.raw_call("ep_setup_ex", ctypes.byref(ctypes.c_void_p()), 1, 100, 8, 3, 0, 1.0, 10, 2,
+                     None, 0, None, ctypes.byref(o), None)
+    assert rc == ep.EP_EINVAL
+    assert "solver" in ep.ep_last_error() or "option" in ep.ep_last_error()

@@ -1,0 +1,142 @@
+"""The two setup eigensolvers (full divide-and-conquer, and the
+Chebyshev-filtered subspace iteration with Rayleigh-Ritz and locking)
+against the fp64 oracle's eigh of K_s and against each other.
+
+Both work in float64 on the same K_s, so eigenvalues agree to ~1e-10
+relative; V is handed back in float32, so V D V^T agrees to float32
+rounding. Setup scalars (beta, m*) are compared at 1e-6 as elsewhere.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_common import kernel_id, lowrank, rel
+
+DENSE, SUBSPACE = 1, 2
+
+
+def _setup(X, cfg, r, **opts):
+    import torch
+    import paper_1806_06144_amd as ep
+    Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).to("cuda:0")
+    ctx, info = ep.ep_setup_ex(Xd, X.shape[0], X.shape[1], cfg.l, cfg.kernel, cfg.bandwidth,
+                               cfg.s, cfg.k, sub_idx=r, opts=opts)
+    try:
+        sigma, D, V, _ = ep.ep_get_preconditioner(ctx, info)
+    finally:
+        ep.ep_destroy(ctx)
+    return info, sigma, D, V
+
+
+def _agree(a, b, sig_rtol=1e-10, lr_tol=1e-6):
+    (ia, sa, Da, Va), (ib, sb, Db, Vb) = a, b
+    np.testing.assert_allclose(sa, sb, rtol=sig_rtol)
+    if Va.shape[1]:
+        assert rel(lowrank(Va, Da), lowrank(Vb, Db)) < lr_tol
+    assert ia.beta == pytest.approx(ib.beta, rel=1e-6)
+    assert ia.m_star == pytest.approx(ib.m_star, rel=1e-6)
+
+
+def _against_oracle(res, st, sig_rtol=1e-9):
+    info, sigma, D, V = res
+    np.testing.assert_allclose(sigma, st.sigma, rtol=sig_rtol)
+    if st.k:
+        assert rel(lowrank(V, D), lowrank(st.V, st.D)) < 1e-6
+    assert info.beta == pytest.approx(st.beta, rel=1e-6)
+    assert info.m_star == pytest.approx(st.m_star, rel=1e-6)
+    assert abs(info.m - st.m) <= 1
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("name,k", [("mnist", 160), ("mnist", 0), ("timit", 40)])
+def test_subspace_and_dense_match_oracle(name, k):
+    cfg = synth.get_config(name, n=6000, s=4000, k=k)
+    X = synth.features(cfg, 0)
+    r = synth.subsample_indices(cfg, 0)
+    st = oracle.setup(X, kernel_id(cfg.kernel), cfg.bandwidth, cfg.s, cfg.k, r)
+    sub = _setup(X, cfg, r, solver="subspace", no_fallback=1)
+    den = _setup(X, cfg, r, solver="dense")
+    assert sub[0].solver == SUBSPACE and den[0].solver == DENSE
+    assert 0 < sub[0].eig_residual <= 1e-11 and sub[0].solver_iters >= 1
+    assert sub[0].solver_matvecs >= cfg.k + 1
+    _against_oracle(sub, st)
+    _against_oracle(den, st)
+    _agree(sub, den)
+    # the default picks the subspace solver at this size
+    auto = _setup(X, cfg, r)
+    assert auto[0].solver == SUBSPACE
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+def test_subspace_laplacian():
+    """Laplacian kernel (CIFAR-shaped rows): the two solvers agree tightly;
+    against the oracle, whose Laplacian K_s carries ~1e-8 of rounding on its
+    diagonal (square root of an expanded distance), at 1e-6."""
+    cfg = synth.get_config("cifar", n=4000, s=3000, k=120)
+    X = synth.features(cfg, 0)
+    r = synth.subsample_indices(cfg, 0)
+    st = oracle.setup(X, kernel_id(cfg.kernel), cfg.bandwidth, cfg.s, cfg.k, r)
+    sub = _setup(X, cfg, r, solver="subspace", no_fallback=1)
+    den = _setup(X, cfg, r, solver="dense")
+    _agree(sub, den)
+    _against_oracle(sub, st, sig_rtol=1e-6)
+
+
+@pytest.mark.gpu
+def test_subspace_block_is_whole_space():
+    """k+1+guard >= s: the block spans R^s and one Rayleigh-Ritz is exact."""
+    cfg = synth.get_config("tiny", n=600, s=256, k=200)
+    X = synth.features(cfg, 0)
+    r = synth.subsample_indices(cfg, 0)
+    st = oracle.setup(X, kernel_id(cfg.kernel), cfg.bandwidth, cfg.s, cfg.k, r)
+    sub = _setup(X, cfg, r, solver="subspace", no_fallback=1)
+    assert sub[0].solver == SUBSPACE
+    _against_oracle(sub, st)
+    # the default takes the dense solver for small s
+    assert _setup(X, cfg, r)[0].solver == DENSE
+
+
+@pytest.mark.gpu
+def test_subspace_not_converged():
+    """A bound no iterate can meet: EP_ENUMERIC when fallback is off, the
+    dense solver's result when it is on."""
+    import paper_1806_06144_amd as ep
+    cfg = synth.get_config("tiny", n=2000, s=500, k=20)
+    X = synth.features(cfg, 0)
+    r = synth.subsample_indices(cfg, 0)
+    with pytest.raises(ep.EigenProError) as e:
+        _setup(X, cfg, r, solver="subspace", tol=1e-300, max_iters=2, no_fallback=1)
+    assert e.value.code == ep.EP_ENUMERIC
+    st = oracle.setup(X, kernel_id(cfg.kernel), cfg.bandwidth, cfg.s, cfg.k, r)
+    fb = _setup(X, cfg, r, solver="subspace", tol=1e-300, max_iters=2)
+    assert fb[0].solver == DENSE
+    _against_oracle(fb, st)
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", ["timit", "imagenet"])
+def test_subspace_full_size_setup(name):
+    """The subsample size and rank of the TIMIT- (s = 12000, k = 160) and
+    ImageNet-shaped (s = 20000, k = 200) workloads: subsample rows drawn from
+    the workload's law (the first s rows, taken as the subsample), both
+    solvers, and the eigen-residual of the subspace result against the
+    oracle's float64 K_s."""
+    base = synth.get_config(name)
+    cfg = synth.get_config(name, n=base.s)
+    X = synth.features(cfg, 0)
+    r = np.arange(cfg.s, dtype=np.int64)
+    sub = _setup(X, cfg, r, solver="subspace", no_fallback=1)
+    den = _setup(X, cfg, r, solver="dense")
+    print(f"{name}: setup dense {den[0].setup_ms:.0f} ms, subspace {sub[0].setup_ms:.0f} ms "
+          f"({sub[0].solver_iters} iterations, {sub[0].solver_matvecs} products, "
+          f"residual {sub[0].eig_residual:.2e})", flush=True)
+    _agree(sub, den, sig_rtol=1e-9)
+    Ks = oracle.kernel_matrix(X, X, kernel_id(cfg.kernel), cfg.bandwidth)
+    sigma, V = sub[1], sub[3].astype(np.float64)
+    res = Ks @ V - V * sigma[:cfg.k]
+    assert np.linalg.norm(res) / np.linalg.norm(Ks) < 1e-6
