@@ -31,6 +31,7 @@
 #include "ep_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace ep {
 
@@ -133,7 +134,7 @@ struct Stage {
 };
 
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
-__device__ __forceinline__ void kmv_body(const KmvArgs& p) {
+__device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     constexpr int kLds = DC + 4;     // padded LDS row (floats): conflict-free b128 reads
     using St = Stage<DC>;
     __shared__ __attribute__((aligned(16))) float xs[2][kRows][kLds];
@@ -373,15 +374,313 @@ __device__ __forceinline__ void kmv_body(const KmvArgs& p) {
     }
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Position of quad q (four features) of staged row r inside its 32-float
+// LDS row: q ^ swz(r). Rows are unpadded (the direct-to-LDS loads below
+// write 64 lanes x 16 bytes contiguously), so the quads are permuted
+// instead: the 8 (or 16) lanes that one b128 read serves together fall on
+// distinct banks.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Workgroup barrier after this wave's LDS writes (lgkmcnt) and, with
+// VM >= 0, after all but its VM most recent vector-memory operations
+// (direct-to-LDS loads count there). The asm also keeps the compiler from
+// moving memory operations across the barrier.
+template <int VM>
+__device__ __forceinline__ void wg_barrier() {
+    if constexpr (VM == 0) {
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else if constexpr (VM == 3) {
+        asm volatile("s_waitcnt vmcnt(3) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else {
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+}
+
+// The same computation with the feature chunks copied from global memory
+// straight into LDS (buffer_load_dwordx4 ... lds: no staging registers) into
+// four rotating slots, issued three chunks ahead. Each wave reads its
+// operands one group (four MFMAs) ahead, also across the barrier that ends
+// a chunk (the next chunk's slot was published one barrier earlier), so its
+// MFMAs do not wait for LDS after a barrier. Requires the
+// VEC layout (d % 4 == 0, 16-byte aligned rows).
+template <int KIND, int LTW, bool ACC2>
+__device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
+    constexpr int DC = 32;                    // features per chunk (4 groups of 8)
+    constexpr int kSlot = kRows * DC;         // floats per slot (24 KB)
+    static_assert(kRows % 8 == 0 && kRows / 8 == 3 * (kThreads / 64), "3 loads per wave");
+    __shared__ __attribute__((aligned(16))) float xs0[kSlot];
+    __shared__ __attribute__((aligned(16))) float xs1[kSlot];
+    __shared__ __attribute__((aligned(16))) float xs2[kSlot];
+    __shared__ __attribute__((aligned(16))) float xs3[kSlot];
+    __shared__ float kb[kCSub][kQSub][16][64];
+    __shared__ float s_qn[kBM];
+    __shared__ int64_t s_qid[kBM];
+    __shared__ float s_cn[2][kBN];
+    __shared__ int64_t s_cid[2][kBN];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int tq = (int)((p.nq + kBM - 1) / kBM);
+    const int split = (int)blockIdx.x / tq;
+    const int qtile = (int)blockIdx.x - split * tq;
+    const int64_t q0 = (int64_t)qtile * kBM;
+    const int64_t cb = (int64_t)split * p.cps;
+    const int64_t ce = min(p.nc, cb + p.cps);
+    const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
+    const int nchunk = (int)((p.d + DC - 1) / DC);
+    const int64_t total = ntile * nchunk;
+    const int d = (int)p.d;
+
+    if (tid < kBM) {
+        const int64_t q = q0 + tid;
+        const bool ok = q < p.nq;
+        s_qn[tid] = ok ? p.qn[q] : 0.f;
+        s_qid[tid] = (ok && p.qid) ? p.qid[q] : -1;
+    }
+    auto load_centre_meta = [&](int64_t tile) {
+        if (tid < kBN) {
+            const int64_t c = cb + tile * kBN + tid;
+            const bool ok = c < ce;
+            s_cn[tile & 1][tid] = ok ? p.cn[c] : 0.f;
+            s_cid[tile & 1][tid] = ok ? (p.cid ? p.cid[c] : c) : -2;
+        }
+    };
+    if (ntile > 0) load_centre_meta(0);
+
+    const int qt_s = wave & 1;
+    const int ct_s = wave >> 1;
+    const int gl = wave % p.wl;
+    const int gj = wave / p.wl;
+    const int lb = gl * LTW * kTile;
+    const int lvalid = p.lt * kTile;
+    const bool active = wave < p.wl * p.wj && lb < lvalid;
+
+    floatx16 facc[LTW][kQSub];
+#pragma unroll
+    for (int i = 0; i < LTW; ++i)
+#pragma unroll
+        for (int b = 0; b < kQSub; ++b)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
+    floatx16 sacc, sacc2;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        sacc[v] = 0.f;
+        sacc2[v] = 0.f;
+    }
+
+    // Direct-to-LDS staging: load i (0..2) of this wave fills staged rows
+    // 8j .. 8j+7, j = 3*wave + i (query rows 0..63, then centre rows), one
+    // 16-byte quad per lane: lane L takes row 8j + L/8 and stores at quad
+    // position L%8, i.e. it fetches quad (L%8) ^ swz(row) of that row.
+    const int64_t q_rows = min((int64_t)kBM, p.nq - q0);
+    const __amdgpu_buffer_rsrc_t qrs =
+        make_rsrc(p.Q + q0 * p.ldq, ((q_rows - 1) * p.ldq + p.d) * 4);
+    int dma_voff[3], dma_col[3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        const int j = 3 * wv + i;
+        const int r = 8 * j + (lane >> 3);
+        const int q = (lane & 7) ^ swz(r);
+        dma_col[i] = 4 * q;
+        dma_voff[i] = (r < kBM ? r * (int)p.ldq : (r - kBM) * (int)p.ldc) * 4 + 16 * q;
+    }
+    int64_t pf_tile = 0;
+    int pf_ch = 0;
+    auto slot_of = [&](auto tag) -> float* {
+        constexpr int S = decltype(tag)::value;
+        if constexpr (S == 0) return xs0;
+        else if constexpr (S == 1) return xs1;
+        else if constexpr (S == 2) return xs2;
+        else return xs3;
+    };
+    auto dma = [&](auto tag) {
+        float* base = slot_of(tag);
+        const int64_t c0 = cb + pf_tile * kBN;
+        const __amdgpu_buffer_rsrc_t crs =
+            make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
+        const int kbase = pf_ch * DC;
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            const int j = 3 * wv + i;
+            const int voff = kbase + dma_col[i] < d ? dma_voff[i] : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(j < kBM / 8 ? qrs : crs,
+                                                     (lds_void*)(base + j * 8 * DC), 16, voff,
+                                                     kbase * 4, 0, 0);
+        }
+        if (++pf_ch == nchunk) {
+            pf_ch = 0;
+            ++pf_tile;
+        }
+    };
+
+    // Operand reads: lane (row = lane%32, half h = lane/32) feeds features
+    // 8g+4h .. 8g+4h+3 of group g, as in the staged body.
+    const int h = lane >> 5;
+    const int f = (lane & 7) ^ ((lane >> 3) & 1);     // swz of rows at multiples of 16 + lane%32
+    const int a_off = (kBM + ct_s * 32 + (lane & 31)) * DC;
+    const int b_off = (qt_s * 32 + (lane & 31)) * DC;
+    auto rd = [&](const float* base, int off, int g) {
+        return *reinterpret_cast<const float4*>(base + off + (((2 * g + h) ^ f) << 2));
+    };
+    auto mfma4 = [&](float4 a, float4 b) {
+        if (ACC2) {
+            sacc = mfma(a.x, b.x, sacc);
+            sacc2 = mfma(a.y, b.y, sacc2);
+            sacc = mfma(a.z, b.z, sacc);
+            sacc2 = mfma(a.w, b.w, sacc2);
+        } else {
+            sacc = mfma(a.x, b.x, sacc);
+            sacc = mfma(a.y, b.y, sacc);
+            sacc = mfma(a.z, b.z, sacc);
+            sacc = mfma(a.w, b.w, sacc);
+        }
+    };
+
+    const int w_col = lb + LTW * (lane & 31);
+    const int ldw4 = (int)p.ldw * 4;
+    const int w_voff = w_col < lvalid ? ((lane >> 5) << 2) * ldw4 + w_col * 4 : kOOB;
+    auto w_soff = [&](int jt, int v) { return (jt * 32 + ((v >> 2) << 3) + (v & 3)) * ldw4; };
+
+    int64_t tile = 0;
+    int ch = 0;
+    float4 ra[2], rb[2];      // operand ring: group g in entry g % 2, read one group ahead
+    auto finish_tile = [&]() {
+        const int64_t c0 = cb + tile * kBN;
+        const int bl = qt_s * 32 + (lane & 31);
+        const float qnb = s_qn[bl];
+        const int64_t qidb = s_qid[bl];
+        const float* cn = s_cn[tile & 1];
+        const int64_t* cid = s_cid[tile & 1];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int jl = ct_s * 32 + acc_row(v, lane);
+            const float dot = ACC2 ? sacc[v] + sacc2[v] : sacc[v];
+            float kv = kernel_value<KIND>(qnb + cn[jl] - 2.f * dot, p.scale);
+            if (qidb == cid[jl]) kv = 1.f;
+            if (c0 + jl >= ce) kv = 0.f;
+            kb[ct_s][qt_s][v][lane] = kv;
+            sacc[v] = 0.f;
+            sacc2[v] = 0.f;
+        }
+        if (tile + 1 < ntile) load_centre_meta(tile + 1);
+        wg_barrier<-1>();
+        if (active) {
+            const __amdgpu_buffer_rsrc_t wrs =
+                make_rsrc(p.W + c0 * p.ldw, (int64_t)kBN * p.ldw * 4);
+            float acur[LTW], anxt[LTW];
+            load_w<LTW>(wrs, w_voff, w_soff(gj, 0), acur);
+            for (int jt = gj; jt < kCSub; jt += p.wj) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    if (v < 15)
+                        load_w<LTW>(wrs, w_voff, w_soff(jt, v + 1), anxt);
+                    else if (jt + p.wj < kCSub)
+                        load_w<LTW>(wrs, w_voff, w_soff(jt + p.wj, 0), anxt);
+                    const float k0v = kb[jt][0][v][lane];
+                    const float k1v = kb[jt][1][v][lane];
+#pragma unroll
+                    for (int i = 0; i < LTW; ++i) {
+                        facc[i][0] = mfma(acur[i], k0v, facc[i][0]);
+                        facc[i][1] = mfma(acur[i], k1v, facc[i][1]);
+                    }
+#pragma unroll
+                    for (int i = 0; i < LTW; ++i) acur[i] = anxt[i];
+                }
+            }
+        }
+    };
+
+    // One chunk on slot S: its direct loads for chunk it+3 go to slot
+    // S+3 (mod 4), whose chunk (it-1) every wave finished reading before the
+    // previous barrier.
+    auto step = [&](auto tag, int64_t it) {
+        constexpr int S = decltype(tag)::value;
+        if (it + 3 < total) dma(std::integral_constant<int, (S + 3) & 3>{});
+        const float* cur = slot_of(tag);
+        const float* nxt = slot_of(std::integral_constant<int, (S + 1) & 3>{});
+        ra[1] = rd(cur, a_off, 1);
+        rb[1] = rd(cur, b_off, 1);
+        mfma4(ra[0], rb[0]);
+        ra[0] = rd(cur, a_off, 2);
+        rb[0] = rd(cur, b_off, 2);
+        mfma4(ra[1], rb[1]);
+        ra[1] = rd(cur, a_off, 3);
+        rb[1] = rd(cur, b_off, 3);
+        mfma4(ra[0], rb[0]);
+        // first group of chunk it+1, whichever tile it belongs to (after the
+        // last chunk this reads a stale slot, unused)
+        ra[0] = rd(nxt, a_off, 0);
+        rb[0] = rd(nxt, b_off, 0);
+        mfma4(ra[1], rb[1]);
+        // keep each group's reads ahead of the previous group's MFMAs (the
+        // scheduler would otherwise sink them to save eight registers)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // 2 LDS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);   // 4 MFMAs
+        }
+        if (++ch == nchunk) {
+            finish_tile();
+            ++tile;
+            ch = 0;
+        }
+        // chunk it+2 (loaded one step ago) is complete in every wave and
+        // published; this chunk's slot is free for the next step's loads
+        if (it + 3 < total) wg_barrier<3>();
+        else wg_barrier<0>();
+    };
+
+    // prologue: chunks 0..2 into slots 0..2; 0 and 1 must be visible
+    if (total > 0) dma(std::integral_constant<int, 0>{});
+    if (total > 1) dma(std::integral_constant<int, 1>{});
+    if (total > 2) {
+        dma(std::integral_constant<int, 2>{});
+        wg_barrier<3>();
+    } else {
+        wg_barrier<0>();
+    }
+    ra[0] = rd(xs0, a_off, 0);
+    rb[0] = rd(xs0, b_off, 0);
+    for (int64_t it0 = 0; it0 < total; it0 += 4) {
+        step(std::integral_constant<int, 0>{}, it0);
+        if (it0 + 1 < total) step(std::integral_constant<int, 1>{}, it0 + 1);
+        if (it0 + 2 < total) step(std::integral_constant<int, 2>{}, it0 + 2);
+        if (it0 + 3 < total) step(std::integral_constant<int, 3>{}, it0 + 3);
+    }
+
+    if (active) {
+        const int slice = split * p.wj + gj;
+        float* o = p.out + ((int64_t)slice * p.out_rows + q0) * p.ldw;
+#pragma unroll
+        for (int b = 0; b < kQSub; ++b) {
+            const int64_t row = b * 32 + (lane & 31);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int col = lb + LTW * acc_row(v, lane);
+#pragma unroll
+                for (int i = 0; i < LTW; ++i)
+                    if (col + i < lvalid) o[row * p.ldw + col + i] = facc[i][b][v];
+            }
+        }
+    }
+}
+
 // Two entry points with one body, so that profiles tell the predictions pass
 // (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
-    kmv_body<KIND, LTW, VEC, PF, DC, ACC2>(p);
+    if constexpr (VEC) kmv_body_dma<KIND, LTW, ACC2>(p);
+    else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
-    kmv_body<KIND, LTW, VEC, PF, DC, ACC2>(p);
+    if constexpr (VEC) kmv_body_dma<KIND, LTW, ACC2>(p);
+    else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 
 typedef void (*KmvFn)(KmvArgs);
