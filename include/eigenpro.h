@@ -107,7 +107,8 @@ typedef struct ep_setup_opts {
  *   X          device, n x d, row-major float32 training features (the
  *              kernel centres). BORROWED: never copied, must stay alive and
  *              unchanged until ep_destroy.
- *   n, d, l    centres, feature dimension, label columns; each >= 1.
+ *   n, d, l    centres, feature dimension, label columns; each >= 1,
+ *              d <= 2^20.
  *   kernel     EP_GAUSSIAN or EP_LAPLACIAN; bandwidth > 0 and finite.
  *   s, k       subsample size and preconditioner rank, 0 <= k < s <= n.
  *              The top k+1 eigenpairs of K_s = [k(x_ri, x_rj)] are computed;

@@ -119,7 +119,7 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
             int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed,
             bool subsample) {
     *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
-    KmvPlan plan = kmv_plan(nq, nc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
+    KmvPlan plan = kmv_plan(nq, nc, ldc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
     *slices = plan.slices();
     HIP_TRY(c->part.ensure((size_t)plan.slices() * (size_t)(*rows_pad) * c->l_pad * sizeof(float)));
     KmvArgs a{};
@@ -466,6 +466,8 @@ int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int ke
     *out = nullptr;
     if (!X) return fail(EP_EINVAL, "X is NULL");
     if (n < 1 || d < 1 || l < 1) return fail(EP_EINVAL, "need n, d, l >= 1");
+    if (d > (int64_t(1) << 20))
+        return fail(EP_EINVAL, "d = %lld exceeds 2^20 features", (long long)d);
     if (!(0 <= k && k < s && s <= n)) return fail(EP_EINVAL, "need 0 <= k < s <= n");
     if (kernel != EP_GAUSSIAN && kernel != EP_LAPLACIAN)
         return fail(EP_EINVAL, "unknown kernel id %d", kernel);

@@ -53,7 +53,7 @@ struct KmvPlan {
     int64_t cps;
     int slices() const { return splits * wj; }
 };
-KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices);
+KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices);
 // Launches one fused pass per block of up to 1024 label columns. `subsample`
 // selects the entry point used for the subsample pass (same code, its own
 // symbol in profiles).

@@ -62,8 +62,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* base, i
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, (int)bytes,
                                              0x00020000);
 }
-// A per-lane offset that no descriptor reaches (descriptor extents are
-// bounded by 2^30 bytes on the host): the load returns zero. Offsets are
+// A per-lane offset that no descriptor reaches (the host keeps every
+// descriptor's extent below it: query tiles by the limit on d, centre
+// ranges by the split planner): the load returns zero. Offsets are
 // split into a per-lane part (voffset) and a wave-uniform part (soffset,
 // held in a scalar register); a lane's voffset alone already decides
 // whether it is in range.
@@ -727,7 +728,7 @@ float kernel_scale(int kind, float bandwidth) {
     return (float)(-log2e / bw);
 }
 
-KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices) {
+KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices) {
     KmvPlan best{};
     const int lt = (int)std::min<int64_t>(ldw / kTile, 32);
     // contraction layout (label groups wl x centre groups wj = 8 waves):
@@ -750,13 +751,18 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldw, int kind, int max_slices) 
     const int64_t tq = ceil_div(std::max<int64_t>(nq, 1), kBM);
     const int64_t nct = ceil_div(std::max<int64_t>(nc, 1), kBN);
     // splits of the centre axis: minimise the makespan of tq * splits equal
-    // workgroups over the resident slots
+    // workgroups over the resident slots. A split's centre rows must stay
+    // below the buffer-descriptor reach kOOB (loads at kOOB must fall
+    // outside every descriptor), which may force more splits than
+    // max_slices asks for.
+    const int64_t max_per = std::max<int64_t>(1, (int64_t)kOOB / (kBN * std::max<int64_t>(ldc, 1) * 4));
+    const int64_t min_p = ceil_div(nct, max_per);
     int64_t best_p = 1, best_per = nct;
     double best_t = 1e300;
-    for (int64_t P = 1; P <= nct && P * best.wj <= max_slices; ++P) {
+    for (int64_t P = min_p; P <= nct && (P == min_p || P * best.wj <= max_slices); ++P) {
         const int64_t per = ceil_div(nct, P);
         const int64_t peff = ceil_div(nct, per);
-        if (peff != P) continue;
+        if (peff != P || per > max_per) continue;
         const int64_t rounds = ceil_div(tq * peff, slots);
         const double t = (double)rounds * (double)(per + 1);
         if (t < best_t) {

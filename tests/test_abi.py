@@ -36,7 +36,7 @@ def _setup_rc(**kw):
 
 @pytest.mark.parametrize("kw", [
     dict(ctx=None), dict(X=None), dict(n=0), dict(d=0), dict(l=0),
-    dict(k=10), dict(k=-1), dict(s=101), dict(kernel=2), dict(bw=0.0),
+    dict(k=10), dict(k=-1), dict(s=101), dict(kernel=2), dict(bw=0.0), dict(d=(1 << 20) + 1),
     dict(bw=float("nan")), dict(bw=float("inf")), dict(bw=-1.0),
 ])
 def test_setup_rejects_bad_arguments(kw):
