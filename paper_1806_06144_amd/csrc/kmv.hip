@@ -550,6 +550,15 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
     int64_t tile = 0;
     int ch = 0;
     float4 ra[2], rb[2];      // operand ring: group g in entry g % 2, read one group ahead
+    // Contraction weights in flight: PD k-steps ahead. With few labels per
+    // wave (LTW <= 2) a k-step is only 2*LTW MFMAs, too short to cover a
+    // global load, so all 16 fragments of a centre sub-tile are kept in
+    // flight, the first 16 issued during the tile's last chunk.
+    constexpr int PD = LTW <= 2 ? 16 : 1;
+    float wbuf[PD][LTW];
+    auto w_rsrc = [&](int64_t t) {
+        return make_rsrc(p.W + (cb + t * kBN) * p.ldw, (int64_t)kBN * p.ldw * 4);
+    };
     auto finish_tile = [&]() {
         const int64_t c0 = cb + tile * kBN;
         const int bl = qt_s * 32 + (lane & 31);
@@ -571,17 +580,18 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
         if (tile + 1 < ntile) load_centre_meta(tile + 1);
         wg_barrier<-1>();
         if (active) {
-            const __amdgpu_buffer_rsrc_t wrs =
-                make_rsrc(p.W + c0 * p.ldw, (int64_t)kBN * p.ldw * 4);
-            float acur[LTW], anxt[LTW];
-            load_w<LTW>(wrs, w_voff, w_soff(gj, 0), acur);
+            const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
+            if constexpr (PD == 1) load_w<LTW>(wrs, w_voff, w_soff(gj, 0), wbuf[0]);
             for (int jt = gj; jt < kCSub; jt += p.wj) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    if (v < 15)
-                        load_w<LTW>(wrs, w_voff, w_soff(jt, v + 1), anxt);
-                    else if (jt + p.wj < kCSub)
-                        load_w<LTW>(wrs, w_voff, w_soff(jt + p.wj, 0), anxt);
+                    float acur[LTW];
+#pragma unroll
+                    for (int i = 0; i < LTW; ++i) acur[i] = wbuf[v % PD][i];
+                    // refill the entry with the fragment PD k-steps ahead
+                    const int nv = v + PD < 16 ? v + PD : v + PD - 16;
+                    const int njt = v + PD < 16 ? jt : jt + p.wj;
+                    if (njt < kCSub) load_w<LTW>(wrs, w_voff, w_soff(njt, nv), wbuf[v % PD]);
                     const float k0v = kb[jt][0][v][lane];
                     const float k1v = kb[jt][1][v][lane];
 #pragma unroll
@@ -589,8 +599,6 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
                         facc[i][0] = mfma(acur[i], k0v, facc[i][0]);
                         facc[i][1] = mfma(acur[i], k1v, facc[i][1]);
                     }
-#pragma unroll
-                    for (int i = 0; i < LTW; ++i) acur[i] = anxt[i];
                 }
             }
         }
@@ -604,6 +612,13 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
         if (it + 3 < total) dma(std::integral_constant<int, (S + 3) & 3>{});
         const float* cur = slot_of(tag);
         const float* nxt = slot_of(std::integral_constant<int, (S + 1) & 3>{});
+        if constexpr (PD == 16) {
+            if (ch + 1 == nchunk && active) {
+                const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+            }
+        }
         ra[1] = rd(cur, a_off, 1);
         rb[1] = rd(cur, b_off, 1);
         mfma4(ra[0], rb[0]);
