@@ -246,13 +246,40 @@ int ep_set_checks(ep_ctx* ctx, int on);
  * ep_timing_enable(ctx, 1) starts recording and clears totals;
  * ep_timing_read synchronises the stream and returns the totals in ms. */
 typedef struct ep_timing {
-    double kmv_ms;          /* sum over launches of the step-2 kernel */
-    int64_t kmv_launches;
+    double kmv_ms;          /* sum over steps of the step-2 pass
+                               F = K(X_t, X) alpha (one fused launch, or all
+                               launches of the blocked form)               */
+    int64_t kmv_launches;   /* number of step-2 passes timed               */
     double step_ms;         /* sum over ep_step calls */
     int64_t steps;
+    double kblock_ms;       /* blocked form only: sum over launches of the
+                               kernel-block kernel (distances -> kernel
+                               values of one centre chunk)                 */
+    int64_t kblock_launches;
+    double gemm_ms;         /* blocked form only: sum over the contraction
+                               GEMMs F += K_chunk alpha_chunk              */
+    int64_t gemm_launches;
 } ep_timing;
 int ep_timing_enable(ep_ctx* ctx, int on);
 int ep_timing_read(ep_ctx* ctx, ep_timing* out);
+
+/* How F = K(Z, X) alpha is formed (Algorithm 1 step 2, prediction):
+ *   EP_CONTRACT_FUSED    one kernel produces kernel values tile by tile in
+ *                        registers and contracts them with alpha at once;
+ *                        the kernel block never reaches memory.
+ *   EP_CONTRACT_BLOCKED  the paper's order of work, one centre chunk at a
+ *                        time: a kernel writes the chunk's kernel block
+ *                        (at most 2 GiB), then a GEMM adds block x alpha
+ *                        chunk into F. Needs d % 4 == 0 and 16-byte aligned
+ *                        rows (else the fused form runs).
+ *   EP_CONTRACT_AUTO     the blocked form when it applies and l >= 256
+ *                        (many label columns make the fused form's
+ *                        accumulators crowd out its distance tile), else
+ *                        the fused form. Default.
+ * Both forms give the same values up to float32 summation order. The
+ * subsample pass of steps 4-5 always uses the fused form. */
+enum { EP_CONTRACT_AUTO = 0, EP_CONTRACT_FUSED = 1, EP_CONTRACT_BLOCKED = 2 };
+int ep_set_contraction(ep_ctx* ctx, int mode);
 
 /* Device probe (no context): runs a register-only kernel of independent
  * fp32 MFMA chains (v_mfma_f32_32x32x2f32, two waves per SIMD on every CU)

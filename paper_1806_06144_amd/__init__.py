@@ -20,6 +20,9 @@ HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "eigenpro.h")
 EP_OK, EP_EINVAL, EP_ENOMEM, EP_EDEVICE, EP_ENUMERIC, EP_EINDEX = 0, -1, -2, -3, -4, -5
 EP_GAUSSIAN, EP_LAPLACIAN = 0, 1
 EP_SOLVER_AUTO, EP_SOLVER_DENSE, EP_SOLVER_SUBSPACE = 0, 1, 2
+EP_CONTRACT_AUTO, EP_CONTRACT_FUSED, EP_CONTRACT_BLOCKED = 0, 1, 2
+CONTRACTIONS = {"auto": EP_CONTRACT_AUTO, "fused": EP_CONTRACT_FUSED,
+                "blocked": EP_CONTRACT_BLOCKED}
 SOLVERS = {"auto": EP_SOLVER_AUTO, "dense": EP_SOLVER_DENSE, "subspace": EP_SOLVER_SUBSPACE}
 KERNELS = {"gaussian": EP_GAUSSIAN, "laplacian": EP_LAPLACIAN}
 _CODES = {EP_EINVAL: "EP_EINVAL", EP_ENOMEM: "EP_ENOMEM", EP_EDEVICE: "EP_EDEVICE",
@@ -49,7 +52,9 @@ class EpSetupOpts(ctypes.Structure):
 
 class EpTiming(ctypes.Structure):
     _fields_ = [("kmv_ms", ctypes.c_double), ("kmv_launches", ctypes.c_int64),
-                ("step_ms", ctypes.c_double), ("steps", ctypes.c_int64)]
+                ("step_ms", ctypes.c_double), ("steps", ctypes.c_int64),
+                ("kblock_ms", ctypes.c_double), ("kblock_launches", ctypes.c_int64),
+                ("gemm_ms", ctypes.c_double), ("gemm_launches", ctypes.c_int64)]
 
 
 class EigenProError(RuntimeError):
@@ -61,7 +66,7 @@ class EigenProError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
-                          "or python -m paper_1806_06144_amd.build")
+                          "or python paper_1806_06144_amd/build.py")
     # torch ships its own HIP runtime under the same soname; loading torch
     # first makes the library bind to that one, so the process holds a
     # single runtime (two copies would not see each other's devices).
@@ -84,6 +89,7 @@ def _load():
         "ep_get_info": (I, [P, ctypes.POINTER(EpInfo)]),
         "ep_set_checks": (I, [P, I]),
         "ep_set_rank": (I, [P, I64]),
+        "ep_set_contraction": (I, [P, I]),
         "ep_adapt": (I, [P, I64, ctypes.POINTER(EpInfo)]),
         "ep_batch_sweep": (I, [P, P, I, I, P]),
         "ep_resource_batch": (I, [P, ctypes.c_double, ctypes.POINTER(I64), ctypes.POINTER(I64),
@@ -254,6 +260,13 @@ def ep_get_info(ctx):
 
 def ep_set_rank(ctx, k):
     return _check(_lib.ep_set_rank(ctx, k))
+
+
+def ep_set_contraction(ctx, mode):
+    """mode: EP_CONTRACT_* or "auto" / "fused" / "blocked"."""
+    if isinstance(mode, str):
+        mode = CONTRACTIONS[mode]
+    return _check(_lib.ep_set_contraction(ctx, mode))
 
 
 def ep_adapt(ctx, m_G):

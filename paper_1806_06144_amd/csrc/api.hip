@@ -72,8 +72,12 @@ struct ep_ctx {
     DevBuf xb, xb_norms, R, part, G, vt_part, W1, zn;
 
     bool timing = false;
-    std::vector<TimedPair> kmv_ev, step_ev;
+    std::vector<TimedPair> kmv_ev, step_ev, kblk_ev, gemm_ev;
     ep_timing tsum{};
+
+    int contract = EP_CONTRACT_AUTO;    // ep_set_contraction
+    rocblas_handle blas = nullptr;      // for the blocked form's GEMMs
+    DevBuf kbuf;                        // one centre chunk's kernel block
 
     ~ep_ctx() {
         for (DevBuf* b : {&norms, &alpha, &r_dev, &Xs, &xs_norms, &V, &Dk, &err, &xb, &xb_norms,
@@ -83,10 +87,12 @@ struct ep_ctx {
             (void)hipEventDestroy(p.a);
             (void)hipEventDestroy(p.b);
         }
-        for (auto& p : step_ev) {
-            (void)hipEventDestroy(p.a);
-            (void)hipEventDestroy(p.b);
-        }
+        for (auto* v : {&step_ev, &kblk_ev, &gemm_ev})
+            for (auto& p : *v) {
+                (void)hipEventDestroy(p.a);
+                (void)hipEventDestroy(p.b);
+            }
+        if (blas) rocblas_destroy_handle(blas);
     }
 };
 
@@ -151,6 +157,86 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
         if (rc) return rc;
     }
     return EP_OK;
+}
+
+constexpr size_t kKBlockBudget = size_t(2) << 30;   // bytes of one chunk's kernel block
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Whether F = K(Q, X) alpha takes the blocked form (see ep_set_contraction).
+bool use_blocked(const ep_ctx* c, const float* Q, int64_t ldq) {
+    if (c->contract == EP_CONTRACT_FUSED) return false;
+    const bool ok = c->d % 4 == 0 && ldq % 4 == 0 && aligned16(Q) && aligned16(c->X);
+    if (!ok) return false;
+    return c->contract == EP_CONTRACT_BLOCKED || c->l >= 256;
+}
+
+// F = K(Q, X) alpha in the blocked form: per chunk of centres, the kernel
+// block (kblock.hip), then F += block . alpha_chunk as a float32 GEMM
+// (rocBLAS, column-major view: F^T = alpha_chunk^T . block^T). F goes to
+// slice 0 of c->part (rows_pad x l_pad).
+int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
+                int64_t nq, int* slices, int64_t* rows_pad, bool timed) {
+    hipStream_t st = c->stream;
+    *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
+    *slices = 1;
+    HIP_TRY(c->part.ensure((size_t)(*rows_pad) * c->l_pad * sizeof(float)));
+    const int64_t rows256 = round_up(nq, 256);
+    int64_t ldo = (int64_t)(kKBlockBudget / ((size_t)rows256 * sizeof(float))) / 256 * 256;
+    ldo = std::max<int64_t>(256, std::min<int64_t>(ldo, round_up(c->n, 256)));
+    HIP_TRY(c->kbuf.ensure((size_t)rows256 * ldo * sizeof(float)));
+    if (!c->blas) {
+        if (rocblas_create_handle(&c->blas) != rocblas_status_success) {
+            c->blas = nullptr;
+            return fail(EP_EDEVICE, "rocblas_create_handle failed");
+        }
+    }
+    rocblas_set_stream(c->blas, st);
+    int rc = EP_OK;
+    if (timed && (rc = record(st, c->kmv_ev, true))) return rc;
+    for (int64_t cs = 0; cs < c->n; cs += ldo) {
+        const int64_t nc = std::min(ldo, c->n - cs);
+        KblockArgs a{};
+        a.Q = Q;
+        a.ldq = ldq;
+        a.qn = qn;
+        a.qid = qid;
+        a.nq = nq;
+        a.C = c->X + cs * c->d;
+        a.ldc = c->d;
+        a.cn = c->norms.as<float>() + cs;
+        a.cid_base = cs;
+        a.nc = nc;
+        a.d = c->d;
+        a.kind = c->kind;
+        a.scale = c->scale;
+        a.out = c->kbuf.as<float>();
+        a.ldo = ldo;
+        if (timed && (rc = record(st, c->kblk_ev, true))) return rc;
+        HIP_TRY(kblock_launch(a, st));
+        if (timed && (rc = record(st, c->kblk_ev, false))) return rc;
+        if (timed && (rc = record(st, c->gemm_ev, true))) return rc;
+        const float one = 1.f, beta = cs == 0 ? 0.f : 1.f;
+        const rocblas_status gs = rocblas_sgemm(
+            c->blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)c->l_pad,
+            (rocblas_int)nq, (rocblas_int)nc, &one, c->alpha.as<float>() + cs * c->l_pad,
+            (rocblas_int)c->l_pad, c->kbuf.as<float>(), (rocblas_int)ldo, &beta,
+            c->part.as<float>(), (rocblas_int)c->l_pad);
+        if (gs != rocblas_status_success)
+            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        if (timed && (rc = record(st, c->gemm_ev, false))) return rc;
+    }
+    if (timed && (rc = record(st, c->kmv_ev, false))) return rc;
+    return EP_OK;
+}
+
+// F = K(Q, X) alpha over all training points: blocked or fused form.
+int run_main_pass(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
+                  int64_t nq, int* slices, int64_t* rows_pad, bool timed) {
+    if (use_blocked(c, Q, ldq))
+        return run_blocked(c, Q, ldq, qn, qid, nq, slices, rows_pad, timed);
+    return run_kmv(c, Q, ldq, qn, qid, nq, c->X, c->d, c->norms.as<float>(), nullptr, c->n,
+                   c->alpha.as<float>(), slices, rows_pad, timed, false);
 }
 
 struct DeviceGuard {
@@ -580,8 +666,7 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     // step 2: F = K(X_t, X) alpha, fused
     int slices = 0;
     int64_t rows_pad = 0;
-    rc = run_kmv(c, xb, c->d, xbn, t, m, c->X, c->d, c->norms.as<float>(), nullptr, c->n, alpha,
-                 &slices, &rows_pad, c->timing, false);
+    rc = run_main_pass(c, xb, c->d, xbn, t, m, &slices, &rows_pad, c->timing);
     if (rc) return rc;
     // step 3: R = F - y_b; alpha_t -= c R
     const double coef = 1.0 / (c->info.beta + (double)(m - 1) * c->info.lambda_k1);
@@ -631,9 +716,8 @@ int ep_predict(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
         HIP_TRY(launch_row_norms(Zc, nz, c->d, c->d, c->zn.as<float>(), st));
         int slices = 0;
         int64_t rows_pad = 0;
-        int rc = run_kmv(c, Zc, c->d, c->zn.as<float>(), nullptr, nz, c->X, c->d,
-                         c->norms.as<float>(), nullptr, c->n, c->alpha.as<float>(), &slices,
-                         &rows_pad, false, false);
+        int rc = run_main_pass(c, Zc, c->d, c->zn.as<float>(), nullptr, nz, &slices, &rows_pad,
+                               false);
         if (rc) return rc;
         HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, nz, c->l,
                                    out + z0 * c->l, c->l, st));
@@ -798,7 +882,7 @@ int ep_timing_enable(ep_ctx* c, int on) {
     if (!c) return fail(EP_EINVAL, "ctx is NULL");
     DeviceGuard dg(c->device);
     HIP_TRY(hipStreamSynchronize(c->stream));
-    for (auto* v : {&c->kmv_ev, &c->step_ev}) {
+    for (auto* v : {&c->kmv_ev, &c->step_ev, &c->kblk_ev, &c->gemm_ev}) {
         for (auto& p : *v) {
             (void)hipEventDestroy(p.a);
             (void)hipEventDestroy(p.b);
@@ -828,7 +912,28 @@ int ep_timing_read(ep_ctx* c, ep_timing* out) {
         t.step_ms += ms;
         t.steps += 1;
     }
+    for (auto& p : c->kblk_ev) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.a, p.b));
+        t.kblock_ms += ms;
+        t.kblock_launches += 1;
+    }
+    for (auto& p : c->gemm_ev) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, p.a, p.b));
+        t.gemm_ms += ms;
+        t.gemm_launches += 1;
+    }
     *out = t;
+    return EP_OK;
+}
+
+int ep_set_contraction(ep_ctx* c, int mode) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (mode < EP_CONTRACT_AUTO || mode > EP_CONTRACT_BLOCKED)
+        return fail(EP_EINVAL, "unknown contraction mode %d", mode);
+    c->contract = mode;
     return EP_OK;
 }
 

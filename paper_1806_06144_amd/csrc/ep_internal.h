@@ -61,6 +61,27 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample
 
 float kernel_scale(int kind, float bandwidth);
 
+// One launch of out[i, j] = k(q_i, c_j) for all nq queries and a chunk of nc
+// centres (kblock.hip). Rows must be 16-byte aligned and d % 4 == 0.
+struct KblockArgs {
+    const float* Q;        // queries, nq x d, leading dimension ldq
+    int64_t ldq;
+    const float* qn;       // |q_i|^2
+    const int64_t* qid;    // global row id of each query (NULL: none)
+    int64_t nq;
+    const float* C;        // centres of the chunk, nc x d, leading dimension ldc
+    int64_t ldc;
+    const float* cn;       // |c_j|^2
+    int64_t cid_base;      // global row id of centre 0 of the chunk
+    int64_t nc;
+    int64_t d;
+    int kind;
+    float scale;
+    float* out;            // row-major, >= round_up(nq, 256) rows x ldo
+    int64_t ldo;           // >= round_up(nc, 256)
+};
+hipError_t kblock_launch(const KblockArgs& a, hipStream_t s);
+
 // Auxiliary kernels (kernels.hip).
 hipError_t launch_row_norms(const float* X, int64_t rows, int64_t d, int64_t ld,
                             float* out, hipStream_t s);

@@ -28,6 +28,7 @@
 //      accumulators of up to 1024 labels fit in 128 registers per lane.
 // Partial sums of each split (and centre group, see wl/wj) are written to
 // their own slice and summed by a separate deterministic reduction.
+#include "ep_device.h"
 #include "ep_internal.h"
 
 #include <algorithm>
@@ -35,40 +36,12 @@
 
 namespace ep {
 
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-
 namespace {
 
 constexpr int kRows = kBM + kBN;     // staged rows per chunk: queries, then centres
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
 
 static_assert(kBM == 64 && kBN == 128 && kThreads == 512, "staging map assumes 64 x 128, 512");
-
-// Row, inside a 32x32 tile, of accumulator element v held by `lane` for the
-// 32x32x2 f32 MFMA; the column is lane % 32. The same map gives the k index
-// a lane feeds at step v when a product's K dimension is read from such an
-// accumulator.
-__device__ __forceinline__ int acc_row(int v, int lane) {
-    return ((v >> 2) << 3) + ((lane >> 5) << 2) + (v & 3);
-}
-
-__device__ __forceinline__ floatx16 mfma(float a, float b, floatx16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-}
-
-// Buffer descriptor over [base, base + bytes): loads at offsets outside it
-// return zero, which provides the zero padding of ragged tiles in hardware.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* base, int64_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, (int)bytes,
-                                             0x00020000);
-}
-// A per-lane offset that no descriptor reaches (the host keeps every
-// descriptor's extent below it: query tiles by the limit on d, centre
-// ranges by the split planner): the load returns zero. Offsets are
-// split into a per-lane part (voffset) and a wave-uniform part (soffset,
-// held in a scalar register); a lane's voffset alone already decides
-// whether it is in range.
-constexpr int kOOB = 0x40000000;
 
 __device__ __forceinline__ float ld1(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
@@ -117,12 +90,6 @@ __device__ __forceinline__ void load_w(__amdgpu_buffer_rsrc_t r, int voff, int s
     }
 }
 
-template <int KIND>
-__device__ __forceinline__ float kernel_value(float d2, float scale) {
-    d2 = fmaxf(d2, 0.f);
-    if (KIND == 0) return __builtin_amdgcn_exp2f(scale * d2);
-    return __builtin_amdgcn_exp2f(scale * __builtin_amdgcn_sqrtf(d2));
-}
 
 // One thread's share of a staged chunk of DC features: NP passes of
 // 512 / (DC/4) rows each over the 64 query rows then the 128 centre rows.
@@ -375,30 +342,6 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     }
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Position of quad q (four features) of staged row r inside its 32-float
-// LDS row: q ^ swz(r). Rows are unpadded (the direct-to-LDS loads below
-// write 64 lanes x 16 bytes contiguously), so the quads are permuted
-// instead: the 8 (or 16) lanes that one b128 read serves together fall on
-// distinct banks.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-// Workgroup barrier after this wave's LDS writes (lgkmcnt) and, with
-// VM >= 0, after all but its VM most recent vector-memory operations
-// (direct-to-LDS loads count there). The asm also keeps the compiler from
-// moving memory operations across the barrier.
-template <int VM>
-__device__ __forceinline__ void wg_barrier() {
-    if constexpr (VM == 0) {
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    } else if constexpr (VM == 3) {
-        asm volatile("s_waitcnt vmcnt(3) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    } else {
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    }
-}
-
 // The same computation with the feature chunks copied from global memory
 // straight into LDS (buffer_load_dwordx4 ... lds: no staging registers) into
 // four rotating slots, issued three chunks ahead. Each wave reads its
@@ -486,7 +429,7 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
     for (int i = 0; i < 3; ++i) {
         const int j = 3 * wv + i;
         const int r = 8 * j + (lane >> 3);
-        const int q = (lane & 7) ^ swz(r);
+        const int q = (lane & 7) ^ swz32(r);
         dma_col[i] = 4 * q;
         dma_voff[i] = (r < kBM ? r * (int)p.ldq : (r - kBM) * (int)p.ldc) * 4 + 16 * q;
     }

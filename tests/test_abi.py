@@ -11,7 +11,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LIB = os.path.join(ROOT, "paper_1806_06144_amd", "libeigenpro.so")
 
 if not os.path.exists(LIB):
-    from paper_1806_06144_amd import build as _b
+    import importlib.util
+    _spec = importlib.util.spec_from_file_location(
+        "_eigenpro_build", os.path.join(ROOT, "paper_1806_06144_amd", "build.py"))
+    _b = importlib.util.module_from_spec(_spec)
+    _spec.loader.exec_module(_b)
     _b.build()
 
 import paper_1806_06144_amd as ep  # noqa: E402
