@@ -34,13 +34,20 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kmv_source_sha():
-    with open(os.path.join(ROOT, "paper_1806_06144_amd", "csrc", "kmv.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+KERNEL_SOURCES = {"kmv_kernel": ["kmv.hip", "ep_device.h"],
+                  "kblock_kernel": ["kblock.hip", "ep_device.h"]}
 
 
-def measured_traffic(workload):
-    """HBM bytes per launch of the fused kernel from committed rocprofv3
+def kernel_source_sha(kernel="kmv_kernel"):
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_1806_06144_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel="kmv_kernel"):
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3
     counter runs, if they were taken on the current kernel source."""
     path = os.path.join(ROOT, "profiles", "kmv_traffic.json")
     try:
@@ -48,8 +55,8 @@ def measured_traffic(workload):
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    entry = rec.get(workload)
-    if not entry or entry.get("kmv_source_sha") != kmv_source_sha():
+    entry = rec.get(f"{workload} | {kernel}")
+    if not entry or entry.get("source_sha") != kernel_source_sha(kernel):
         return None
     return entry.get("bytes_per_launch")
 
@@ -261,7 +268,7 @@ def study_setup(args):
     return out
 
 
-def traffic_summary(fetch_csv, write_csv, workload, command_note):
+def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
     """HBM bytes per launch of the fused kernel from two rocprofv3 --pmc
     runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the
     same counter reads for the 1 GiB device copies of --calibrate-copy.
@@ -277,6 +284,7 @@ def traffic_summary(fetch_csv, write_csv, workload, command_note):
                 name = row["Kernel_Name"]
                 key = ("kmv_kernel" if "kmv_kernel<" in name else
                        "kmv_subsample_kernel" if "kmv_subsample_kernel<" in name else
+                       "kblock_kernel" if "kblock_kernel<" in name else
                        "copy" if "copyBuffer" in name and float(row["Counter_Value"]) > (1 << 18) else
                        None)
                 if key:
@@ -288,7 +296,7 @@ def traffic_summary(fetch_csv, write_csv, workload, command_note):
     gib_kib = float(1 << 20)
     rf = gib_kib / np.mean(fe["copy"])
     wf = gib_kib / np.mean(wr["copy"])
-    f_kib, w_kib = np.mean(fe["kmv_kernel"]), np.mean(wr["kmv_kernel"])
+    f_kib, w_kib = np.mean(fe[kernel]), np.mean(wr[kernel])
     bytes_launch = (f_kib * rf + w_kib * wf) * 1024.0
     rec = {}
     path = os.path.join(ROOT, "profiles", "kmv_traffic.json")
@@ -297,21 +305,22 @@ def traffic_summary(fetch_csv, write_csv, workload, command_note):
             rec = json.load(f)
     except (OSError, ValueError):
         rec = {}
-    rec[workload] = {"kmv_source_sha": kmv_source_sha(), "bytes_per_launch": bytes_launch,
-                     "fetch_kib": f_kib, "write_kib": w_kib, "read_factor": rf,
-                     "write_factor": wf, "summary": "profiles/kmv_imagenet_traffic.txt"}
+    rec[f"{workload} | {kernel}"] = {
+        "source_sha": kernel_source_sha(kernel), "bytes_per_launch": bytes_launch,
+        "fetch_kib": f_kib, "write_kib": w_kib, "read_factor": rf, "write_factor": wf}
     with open(path, "w") as f:
         json.dump(rec, f, indent=1)
-    lines = [f"workload: {workload}", f"kmv.hip sha256[:16]: {kmv_source_sha()}", "",
+    lines = [f"workload: {workload}", f"kernel: {kernel}",
+             f"kernel source sha256[:16]: {kernel_source_sha(kernel)}", "",
              command_note, "", "per-dispatch counter values (KiB):"]
-    for key in ["kmv_kernel", "kmv_subsample_kernel", "copy"]:
+    for key in [kernel, "kmv_subsample_kernel", "copy"]:
         lines.append(f"  {key:21s} FETCH_SIZE " + ", ".join(f"{v:.6g}" for v in fe.get(key, [])))
         lines.append(f"  {key:21s} WRITE_SIZE " + ", ".join(f"{v:.6g}" for v in wr.get(key, [])))
     lines += ["", "calibration: a 1 GiB copy reads and writes 1048576 KiB;",
               f"  read factor  = 1048576 / {np.mean(fe['copy']):.6g} = {rf:.4f}",
               f"  write factor = 1048576 / {np.mean(wr['copy']):.6g} = {wf:.4f}", "",
-              f"kmv_kernel traffic per launch = ({f_kib:.6g} * {rf:.4f} + {w_kib:.6g} * {wf:.4f}) KiB",
-              f"                              = {bytes_launch / 1e9:.1f} GB"]
+              f"{kernel} traffic per launch = ({f_kib:.6g} * {rf:.4f} + {w_kib:.6g} * {wf:.4f}) KiB",
+              f"    = {bytes_launch / 1e9:.2f} GB"]
     return "\n".join(lines)
 
 
@@ -322,6 +331,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="imagenet")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--contraction", choices=["auto", "fused", "blocked"], default="auto",
+                    help="form of F = K(X_t, X) alpha (ep_set_contraction)")
     ap.add_argument("--s", type=int, default=None,
                     help="override the subsample size (experiments only)")
     ap.add_argument("--shard", type=int, default=1,
@@ -345,8 +356,10 @@ def main():
         fcsv, wcsv, bout = args.traffic_summary
         with open(bout) as f:
             line = [x for x in f.read().splitlines() if x.startswith("{")][-1]
-        workload = json.loads(line)["config"]["workload"]
-        print(traffic_summary(fcsv, wcsv, workload,
+        rec = json.loads(line)
+        workload = rec["config"]["workload"]
+        kernel = rec["roofline"]["kernel"].split()[0]
+        print(traffic_summary(fcsv, wcsv, workload, kernel,
                               "counters from rocprofv3 --pmc FETCH_SIZE / --pmc WRITE_SIZE runs of "
                               "bench.py --calibrate-copy (three 1 GiB device copies)"))
         return
@@ -390,6 +403,7 @@ def main():
     if args.save_setup:
         sigma, _, V, r_used = ep.ep_get_preconditioner(ctx, info)
         np.savez(args.save_setup, r=r_used, sigma=sigma, V=V)
+    ep.ep_set_contraction(ctx, args.contraction)
     m = int(cfg.m) if cfg.m else int(info.m)
     log(f"setup {info.setup_ms / 1e3:.1f} s: m*={info.m_star:.1f} m={m} beta={info.beta:.4f} "
         f"sigma_k+1={info.sigma_k1:.4f} eta={info.eta:.1f}")
@@ -422,7 +436,25 @@ def main():
     kmv_flops = 2.0 * m * n * (d + l)
     step_flops = 2.0 * m * (n + s) * (d + l) + 4.0 * s * k * l
     kmv_avg_s = tim.kmv_ms / 1e3 / max(tim.kmv_launches, 1)
-    achieved = kmv_flops / kmv_avg_s / 1e12
+    pass_tflops = kmv_flops / kmv_avg_s / 1e12
+    blocked = tim.kblock_launches > 0
+    if blocked:
+        # dominant kernel: the kernel block (distances -> kernel values);
+        # its algorithmic work is 2 d flops per entry, over all chunks
+        dom = "kblock_kernel"
+        dom_label = "kblock_kernel (distance -> kernel block of a centre chunk, step 2, blocked form)"
+        launches = int(tim.kblock_launches)
+        dom_avg_s = tim.kblock_ms / 1e3 / launches
+        dom_flops = 2.0 * m * n * d * args.steps / launches
+        gemm_tflops = 2.0 * m * n * l * args.steps / (tim.gemm_ms / 1e3) / 1e12
+    else:
+        dom = "kmv_kernel"
+        dom_label = "kmv_kernel (fused distance -> kernel -> contraction, step 2)"
+        launches = int(tim.kmv_launches)
+        dom_avg_s = kmv_avg_s
+        dom_flops = kmv_flops
+        gemm_tflops = None
+    achieved = dom_flops / dom_avg_s / 1e12
     workload = f"{cfg.name}-shaped n={n} d={d} l={l} {cfg.kernel} bw={cfg.bandwidth:g} s={s} k={k} m={m}"
     if args.shard > 1:
         workload += f" (1/{args.shard} centre shard)"
@@ -447,7 +479,7 @@ def main():
         cpu = cpu_baseline(X, alpha.cpu().numpy(), cfg)
     ep.ep_destroy(ctx)
 
-    traffic = measured_traffic(workload)
+    traffic = measured_traffic(workload, dom)
     out = {
         "metric": "kernel entries/s (m*n per step)",
         "value": entries / sec_per_step,
@@ -463,7 +495,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload, "n": n, "d": d, "l": l, "s": s, "k": k, "m": m,
                    "kernel": cfg.kernel, "bandwidth": cfg.bandwidth},
-        "tflops_fused_kernel": achieved,
+        "contraction": "blocked" if blocked else "fused",
+        "tflops_step2_pass": pass_tflops,
+        "tflops_contraction_gemm": gemm_tflops,
         "tflops_whole_step": step_flops / sec_per_step / 1e12,
         "s_per_epoch_est": (n / m) * sec_per_step,
         "setup_s": info.setup_ms / 1e3,
@@ -474,10 +508,10 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
             "traffic": traffic,
-            "kernel": "kmv_kernel (fused distance -> kernel -> contraction, step 2)",
-            "avg_launch_ms": kmv_avg_s * 1e3,
-            "launches": int(tim.kmv_launches),
-            "flops_per_launch": kmv_flops,
+            "kernel": dom_label,
+            "avg_launch_ms": dom_avg_s * 1e3,
+            "launches": launches,
+            "flops_per_launch": dom_flops,
             "probe_mfma_f32_tflops": probe_tf,
             "probe_shader_clock_mhz": probe_mhz,
             "frac_of_probe": achieved / probe_tf if probe_tf > 0 else None,

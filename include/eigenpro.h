@@ -269,8 +269,8 @@ int ep_timing_read(ep_ctx* ctx, ep_timing* out);
  *                        the kernel block never reaches memory.
  *   EP_CONTRACT_BLOCKED  the paper's order of work, one centre chunk at a
  *                        time: a kernel writes the chunk's kernel block
- *                        (at most 2 GiB), then a GEMM adds block x alpha
- *                        chunk into F. Needs d % 4 == 0 and 16-byte aligned
+ *                        (at most block_bytes), then a GEMM adds block x
+ *                        alpha chunk into F. Needs d % 4 == 0 and 16-byte aligned
  *                        rows (else the fused form runs).
  *   EP_CONTRACT_AUTO     the blocked form when it applies and l >= 256
  *                        (many label columns make the fused form's
@@ -279,7 +279,10 @@ int ep_timing_read(ep_ctx* ctx, ep_timing* out);
  * Both forms give the same values up to float32 summation order. The
  * subsample pass of steps 4-5 always uses the fused form. */
 enum { EP_CONTRACT_AUTO = 0, EP_CONTRACT_FUSED = 1, EP_CONTRACT_BLOCKED = 2 };
-int ep_set_contraction(ep_ctx* ctx, int mode);
+/*   block_bytes  upper bound of the blocked form's kernel-block buffer
+ *                (0: 2 GiB); chunks shrink to fit it, down to 256 centres.
+ * Errors: EP_EINVAL for an unknown mode or negative block_bytes. */
+int ep_set_contraction(ep_ctx* ctx, int mode, int64_t block_bytes);
 
 /* Device probe (no context): runs a register-only kernel of independent
  * fp32 MFMA chains (v_mfma_f32_32x32x2f32, two waves per SIMD on every CU)

@@ -89,7 +89,7 @@ def _load():
         "ep_get_info": (I, [P, ctypes.POINTER(EpInfo)]),
         "ep_set_checks": (I, [P, I]),
         "ep_set_rank": (I, [P, I64]),
-        "ep_set_contraction": (I, [P, I]),
+        "ep_set_contraction": (I, [P, I, I64]),
         "ep_adapt": (I, [P, I64, ctypes.POINTER(EpInfo)]),
         "ep_batch_sweep": (I, [P, P, I, I, P]),
         "ep_resource_batch": (I, [P, ctypes.c_double, ctypes.POINTER(I64), ctypes.POINTER(I64),
@@ -262,11 +262,12 @@ def ep_set_rank(ctx, k):
     return _check(_lib.ep_set_rank(ctx, k))
 
 
-def ep_set_contraction(ctx, mode):
-    """mode: EP_CONTRACT_* or "auto" / "fused" / "blocked"."""
+def ep_set_contraction(ctx, mode, block_bytes=0):
+    """mode: EP_CONTRACT_* or "auto" / "fused" / "blocked"; block_bytes: cap
+    of the blocked form's kernel-block buffer (0: 2 GiB)."""
     if isinstance(mode, str):
         mode = CONTRACTIONS[mode]
-    return _check(_lib.ep_set_contraction(ctx, mode))
+    return _check(_lib.ep_set_contraction(ctx, mode, block_bytes))
 
 
 def ep_adapt(ctx, m_G):

@@ -76,6 +76,7 @@ struct ep_ctx {
     ep_timing tsum{};
 
     int contract = EP_CONTRACT_AUTO;    // ep_set_contraction
+    size_t block_bytes = size_t(2) << 30;
     rocblas_handle blas = nullptr;      // for the blocked form's GEMMs
     DevBuf kbuf;                        // one centre chunk's kernel block
 
@@ -172,17 +173,21 @@ bool use_blocked(const ep_ctx* c, const float* Q, int64_t ldq) {
 }
 
 // F = K(Q, X) alpha in the blocked form: per chunk of centres, the kernel
-// block (kblock.hip), then F += block . alpha_chunk as a float32 GEMM
-// (rocBLAS, column-major view: F^T = alpha_chunk^T . block^T). F goes to
-// slice 0 of c->part (rows_pad x l_pad).
+// block (kblock.hip), then float32 GEMMs (rocBLAS, column-major view:
+// F^T = alpha_sub^T . block_sub^T) over sub-ranges of at most kw centres.
+// The sub-range products go round robin to up to 32 partial slices of
+// c->part (beta = 0 on a slice's first use), which the reduction kernels
+// sum: like the fused form's centre splits, this keeps each float32
+// accumulation chain near n / 32 terms instead of n.
 int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
                 int64_t nq, int* slices, int64_t* rows_pad, bool timed) {
     hipStream_t st = c->stream;
     *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
-    *slices = 1;
-    HIP_TRY(c->part.ensure((size_t)(*rows_pad) * c->l_pad * sizeof(float)));
+    const int S = std::max(1, std::min(32, max_slices_for(*rows_pad, c->l_pad)));
+    const int64_t kw = std::max<int64_t>(64, round_up(ceil_div(c->n, S), 64));
+    HIP_TRY(c->part.ensure((size_t)S * (*rows_pad) * c->l_pad * sizeof(float)));
     const int64_t rows256 = round_up(nq, 256);
-    int64_t ldo = (int64_t)(kKBlockBudget / ((size_t)rows256 * sizeof(float))) / 256 * 256;
+    int64_t ldo = (int64_t)(c->block_bytes / ((size_t)rows256 * sizeof(float))) / 256 * 256;
     ldo = std::max<int64_t>(256, std::min<int64_t>(ldo, round_up(c->n, 256)));
     HIP_TRY(c->kbuf.ensure((size_t)rows256 * ldo * sizeof(float)));
     if (!c->blas) {
@@ -192,7 +197,9 @@ int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const i
         }
     }
     rocblas_set_stream(c->blas, st);
+    const size_t slice_elems = (size_t)(*rows_pad) * c->l_pad;
     int rc = EP_OK;
+    int64_t sub = 0;
     if (timed && (rc = record(st, c->kmv_ev, true))) return rc;
     for (int64_t cs = 0; cs < c->n; cs += ldo) {
         const int64_t nc = std::min(ldo, c->n - cs);
@@ -216,17 +223,22 @@ int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const i
         HIP_TRY(kblock_launch(a, st));
         if (timed && (rc = record(st, c->kblk_ev, false))) return rc;
         if (timed && (rc = record(st, c->gemm_ev, true))) return rc;
-        const float one = 1.f, beta = cs == 0 ? 0.f : 1.f;
-        const rocblas_status gs = rocblas_sgemm(
-            c->blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)c->l_pad,
-            (rocblas_int)nq, (rocblas_int)nc, &one, c->alpha.as<float>() + cs * c->l_pad,
-            (rocblas_int)c->l_pad, c->kbuf.as<float>(), (rocblas_int)ldo, &beta,
-            c->part.as<float>(), (rocblas_int)c->l_pad);
-        if (gs != rocblas_status_success)
-            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        for (int64_t k0 = 0; k0 < nc; k0 += kw, ++sub) {
+            const int64_t kk = std::min(kw, nc - k0);
+            const float one = 1.f, beta = sub < S ? 0.f : 1.f;
+            float* out = c->part.as<float>() + (size_t)(sub % S) * slice_elems;
+            const rocblas_status gs = rocblas_sgemm(
+                c->blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)c->l_pad,
+                (rocblas_int)nq, (rocblas_int)kk, &one,
+                c->alpha.as<float>() + (cs + k0) * c->l_pad, (rocblas_int)c->l_pad,
+                c->kbuf.as<float>() + k0, (rocblas_int)ldo, &beta, out, (rocblas_int)c->l_pad);
+            if (gs != rocblas_status_success)
+                return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        }
         if (timed && (rc = record(st, c->gemm_ev, false))) return rc;
     }
     if (timed && (rc = record(st, c->kmv_ev, false))) return rc;
+    *slices = (int)std::min<int64_t>(sub, S);
     return EP_OK;
 }
 
@@ -928,12 +940,14 @@ int ep_timing_read(ep_ctx* c, ep_timing* out) {
     return EP_OK;
 }
 
-int ep_set_contraction(ep_ctx* c, int mode) {
+int ep_set_contraction(ep_ctx* c, int mode, int64_t block_bytes) {
     g_err.clear();
     if (!c) return fail(EP_EINVAL, "ctx is NULL");
     if (mode < EP_CONTRACT_AUTO || mode > EP_CONTRACT_BLOCKED)
         return fail(EP_EINVAL, "unknown contraction mode %d", mode);
+    if (block_bytes < 0) return fail(EP_EINVAL, "block_bytes < 0");
     c->contract = mode;
+    c->block_bytes = block_bytes > 0 ? (size_t)block_bytes : kKBlockBudget;
     return EP_OK;
 }
 

@@ -23,7 +23,7 @@ def kernel_id(name):
 class Gpu:
     """One ep_ctx on cuda:0 over a host feature matrix."""
 
-    def __init__(self, X, l, kernel, bw, s, k, r, seed=0):
+    def __init__(self, X, l, kernel, bw, s, k, r, seed=0, contraction=None, block_bytes=0):
         import torch
         import paper_1806_06144_amd as ep
         self.ep = ep
@@ -34,6 +34,8 @@ class Gpu:
         self.Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).to(self.dev)
         self.ctx, self.info = ep.ep_setup(self.Xd, self.n, self.d, l, kernel, bw, s, k,
                                           sub_idx=r, seed=seed)
+        if contraction is not None:
+            ep.ep_set_contraction(self.ctx, contraction, block_bytes)
 
     def t(self, a):
         return self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
