@@ -49,7 +49,7 @@ def kernel_source_sha(kernel="kmv_kernel"):
 def measured_traffic(workload, kernel="kmv_kernel"):
     """HBM bytes per launch of the dominant kernel from committed rocprofv3
     counter runs, if they were taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "kmv_traffic.json")
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
@@ -272,7 +272,7 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
     """HBM bytes per launch of the fused kernel from two rocprofv3 --pmc
     runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the
     same counter reads for the 1 GiB device copies of --calibrate-copy.
-    Writes profiles/kmv_traffic.json and returns a text summary."""
+    Writes profiles/hbm_traffic.json and returns a text summary."""
     import csv
 
     def per_kernel(path, counter):
@@ -299,7 +299,7 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
     f_kib, w_kib = np.mean(fe[kernel]), np.mean(wr[kernel])
     bytes_launch = (f_kib * rf + w_kib * wf) * 1024.0
     rec = {}
-    path = os.path.join(ROOT, "profiles", "kmv_traffic.json")
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
@@ -346,7 +346,7 @@ def main():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_OUT"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
-                         "WRITE_SIZE; runs with --calibrate-copy) into profiles/kmv_traffic.json "
+                         "WRITE_SIZE; runs with --calibrate-copy) into profiles/hbm_traffic.json "
                          "for the workload named in BENCH_OUT (the JSON line of the counted "
                          "run), and print a summary; no GPU needed")
     ap.add_argument("--study", choices=["batch", "convergence", "setup"], default=None,
