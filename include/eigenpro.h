@@ -272,10 +272,11 @@ int ep_timing_read(ep_ctx* ctx, ep_timing* out);
  *                        (at most block_bytes), then a GEMM adds block x
  *                        alpha chunk into F. Needs d % 4 == 0 and 16-byte aligned
  *                        rows (else the fused form runs).
- *   EP_CONTRACT_AUTO     the blocked form when it applies and l >= 256
- *                        (many label columns make the fused form's
- *                        accumulators crowd out its distance tile), else
- *                        the fused form. Default.
+ *   EP_CONTRACT_AUTO     the fused form (default). The blocked form is
+ *                        faster when it applies and l is large (at
+ *                        l = 1000 the fused form's label accumulators
+ *                        crowd out its distance tile) but writes the block
+ *                        to memory, so it is only taken on request.
  * Both forms give the same values up to float32 summation order. The
  * subsample pass of steps 4-5 always uses the fused form. */
 enum { EP_CONTRACT_AUTO = 0, EP_CONTRACT_FUSED = 1, EP_CONTRACT_BLOCKED = 2 };

@@ -166,10 +166,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 
 // Whether F = K(Q, X) alpha takes the blocked form (see ep_set_contraction).
 bool use_blocked(const ep_ctx* c, const float* Q, int64_t ldq) {
-    if (c->contract == EP_CONTRACT_FUSED) return false;
-    const bool ok = c->d % 4 == 0 && ldq % 4 == 0 && aligned16(Q) && aligned16(c->X);
-    if (!ok) return false;
-    return c->contract == EP_CONTRACT_BLOCKED || c->l >= 256;
+    if (c->contract != EP_CONTRACT_BLOCKED) return false;
+    return c->d % 4 == 0 && ldq % 4 == 0 && aligned16(Q) && aligned16(c->X);
 }
 
 // F = K(Q, X) alpha in the blocked form: per chunk of centres, the kernel
