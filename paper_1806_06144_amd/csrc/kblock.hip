@@ -48,8 +48,8 @@ __global__ void __launch_bounds__(kKThreads) kblock_kernel(KblockArgs p) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wv = wave;
     const int tq = (int)((p.nq + kKM - 1) / kKM);
     const int ctile = (int)blockIdx.x / tq;
     const int qtile = (int)blockIdx.x - ctile * tq;

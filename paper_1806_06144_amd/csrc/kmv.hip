@@ -366,8 +366,13 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    // wave index made visibly uniform: everything derived from it (label
+    // block, centre group, weight offsets) then lives in scalar registers,
+    // and buffer loads need no per-lane offset loops. Not for three label
+    // tiles per wave, whose three separate weight loads the scheduler then
+    // sinks next to their use (measured: a third slower).
+    const int wave = LTW == 3 ? tid >> 6 : __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tq = (int)((p.nq + kBM - 1) / kBM);
     const int split = (int)blockIdx.x / tq;
     const int qtile = (int)blockIdx.x - split * tq;
