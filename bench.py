@@ -373,7 +373,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
-              "this build has no multi-GPU path.", file=sys.stderr)
+              "the library has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -431,6 +431,24 @@ def main():
     ep.ep_sync(ctx)
     tim = ep.ep_timing_read(ctx)
     ep.ep_timing_enable(ctx, False)
+
+    # prediction (Section 2) of held-out rows with the trained alpha: the
+    # same fused pass with m -> n_z, no diagonal rule
+    n_z = 10000 if cfg.n > 100000 else 2000
+    Z = torch.from_numpy(synth.heldout(cfg, 0, n_z=n_z)).to(dev)
+    P = torch.empty((n_z, cfg.l), dtype=torch.float32, device=dev)
+    ep.ep_predict(ctx, Z, n_z, P)
+    ep.ep_sync(ctx)
+    torch.cuda.synchronize()
+    p0 = time.perf_counter()
+    ep.ep_predict(ctx, Z, n_z, P)
+    ep.ep_sync(ctx)
+    p1 = time.perf_counter()
+    predict = {"n_z": n_z, "ms": (p1 - p0) * 1e3,
+               "tflops": 2.0 * n_z * cfg.n * (cfg.d + cfg.l) / (p1 - p0) / 1e12,
+               "entries_per_s": n_z * cfg.n / (p1 - p0)}
+    log(f"predict {n_z} rows: {predict['ms']:.1f} ms, {predict['tflops']:.1f} TFLOP/s")
+    del Z, P
 
     # the blocked form on the same batches, for comparison (not the headline:
     # it writes the kernel block to memory)
@@ -554,6 +572,7 @@ def main():
             "frac_of_probe": achieved / probe_tf if probe_tf > 0 else None,
         },
         "cpu_baseline": cpu,
+        "predict": predict,
         "blocked_form": blocked_form,
     }
     print(json.dumps(out), flush=True)
