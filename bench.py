@@ -268,10 +268,13 @@ def study_setup(args):
     return out
 
 
-def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
-    """HBM bytes per launch of the fused kernel from two rocprofv3 --pmc
+def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note):
+    """HBM bytes per launch of the dominant kernel from two rocprofv3 --pmc
     runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the
     same counter reads for the 1 GiB device copies of --calibrate-copy.
+    Only the kernel's first n_step dispatches count: those of the warm-up
+    and timed steps, whose launches the roofline averages (the prediction
+    pass that follows runs the same kernel on other shapes).
     Writes profiles/hbm_traffic.json and returns a text summary."""
     import csv
 
@@ -293,6 +296,9 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
 
     fe = per_kernel(fetch_csv, "FETCH_SIZE")
     wr = per_kernel(write_csv, "WRITE_SIZE")
+    fe[kernel], wr[kernel] = fe[kernel][:n_step], wr[kernel][:n_step]
+    if len(fe[kernel]) != n_step or len(wr[kernel]) != n_step:
+        raise SystemExit(f"expected {n_step} {kernel} dispatches in each counter run")
     gib_kib = float(1 << 20)
     rf = gib_kib / np.mean(fe["copy"])
     wf = gib_kib / np.mean(wr["copy"])
@@ -312,7 +318,9 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, command_note):
         json.dump(rec, f, indent=1)
     lines = [f"workload: {workload}", f"kernel: {kernel}",
              f"kernel source sha256[:16]: {kernel_source_sha(kernel)}", "",
-             command_note, "", "per-dispatch counter values (KiB):"]
+             command_note, "",
+             f"per-dispatch counter values (KiB; {kernel}: its first {n_step} dispatches, "
+             "those of the warm-up and timed steps):"]
     for key in [kernel, "kmv_subsample_kernel", "copy"]:
         lines.append(f"  {key:21s} FETCH_SIZE " + ", ".join(f"{v:.6g}" for v in fe.get(key, [])))
         lines.append(f"  {key:21s} WRITE_SIZE " + ", ".join(f"{v:.6g}" for v in wr.get(key, [])))
@@ -361,7 +369,8 @@ def main():
         rec = json.loads(line)
         workload = rec["config"]["workload"]
         kernel = rec["roofline"]["kernel"].split()[0]
-        print(traffic_summary(fcsv, wcsv, workload, kernel,
+        n_step = (rec["warmup"] + rec["steps"]) * rec["roofline"]["launches"] // rec["steps"]
+        print(traffic_summary(fcsv, wcsv, workload, kernel, n_step,
                               "counters from rocprofv3 --pmc FETCH_SIZE / --pmc WRITE_SIZE runs of "
                               "bench.py --calibrate-copy (three 1 GiB device copies)"))
         return
