@@ -6,12 +6,14 @@
 
 namespace ep {
 
-// Tile geometry of the fused kernel-block contraction (kmv.hip).
+// Tile geometry of the fused kernel-block contraction (kmv.hip). kBN is
+// also the granularity of centre splits and of the zero padding that weight
+// matrices carry past their last row.
 constexpr int kTile = 32;                 // MFMA 32x32 output tile edge
 constexpr int kQSub = 2;                  // query sub-tiles per workgroup
-constexpr int kCSub = 4;                  // centre sub-tiles per iteration
+constexpr int kCSub = 8;                  // centre sub-tiles per iteration
 constexpr int kBM = kTile * kQSub;        // query rows per workgroup (64)
-constexpr int kBN = kTile * kCSub;        // centres per iteration (128)
+constexpr int kBN = kTile * kCSub;        // centres per iteration (256)
 constexpr int kThreads = 512;             // 8 waves of 64
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }

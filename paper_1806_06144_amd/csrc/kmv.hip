@@ -10,12 +10,16 @@
 // reaches global memory.
 //
 // One workgroup = 8 waves (two per SIMD) owns 64 query rows and a contiguous
-// range of centres (a "split"), walked 128 centres at a time:
+// range of centres (a "split"), walked 256 centres at a time:
 //   1. S = C_tile . Q_tile^T on fp32 MFMA (v_mfma_f32_32x32x2f32): each wave
-//      owns one 32x32 sub-tile of the 128 x 64 block. Features stream
-//      through two LDS slots in chunks of 32; the global loads of a chunk are
-//      issued two chunks ahead (across tile boundaries), so their latency
-//      hides behind two chunks of MFMA work.
+//      owns 32 centres x 64 queries (two 32x32 sub-tiles with independent
+//      accumulators) of the 256 x 64 block. Its centre rows, which no other
+//      wave reads, go from global memory straight into the MFMA operand
+//      registers one batch of 64 features ahead; the query rows, which all
+//      waves read, pass through LDS in batches of 64 features (double
+//      buffered, one barrier per batch). Rows that are not 16-byte aligned
+//      take a register-staged path with 128-centre tiles and LDS for both
+//      sides.
 //   2. Epilogue in registers: d2 = |q|^2 + |c|^2 - 2 S, clamped at 0; then
 //      exp2(scale * d2) (Gaussian) or exp2(scale * sqrt(d2)) (Laplacian).
 //      Where the query and the centre are the same training point the value
@@ -23,9 +27,9 @@
 //   3. The kernel values go to LDS in the MFMA accumulator order, which is
 //      exactly the operand order the second product needs, and
 //      out^T(labels x queries) += W^T(labels x centres) . K(centres x queries)
-//      runs on the same MFMA with W read straight from global memory (one
-//      step ahead). The label tiles are spread over the 8 waves so that the
-//      accumulators of up to 1024 labels fit in 128 registers per lane.
+//      runs on the same MFMA with W read straight from global memory (a few
+//      k-steps ahead). The label tiles are spread over the 8 waves so that
+//      the accumulators of up to 1024 labels fit in 128 registers per lane.
 // Partial sums of each split (and centre group, see wl/wj) are written to
 // their own slice and summed by a separate deterministic reduction.
 #include "ep_device.h"
@@ -39,10 +43,15 @@ namespace ep {
 
 namespace {
 
-constexpr int kRows = kBM + kBN;     // staged rows per chunk: queries, then centres
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
 
-static_assert(kBM == 64 && kBN == 128 && kThreads == 512, "staging map assumes 64 x 128, 512");
+// Register-staged body: 64 queries x 128 centres per iteration.
+constexpr int kSCSub = 4;
+constexpr int kSBN = kTile * kSCSub;
+constexpr int kSRows = kBM + kSBN;   // staged rows per chunk: queries, then centres
+
+static_assert(kBM == 64 && kThreads == 512, "staging maps assume 64 query rows, 512 threads");
+static_assert(kBN == 2 * kSBN, "split granularity serves both bodies");
 
 __device__ __forceinline__ float ld1(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
@@ -98,7 +107,7 @@ template <int DC>
 struct Stage {
     static constexpr int kCols = DC / 4;              // float4 per staged row
     static constexpr int kRowsPerPass = kThreads / kCols;
-    static constexpr int kPasses = kRows / kRowsPerPass;
+    static constexpr int kPasses = kSRows / kRowsPerPass;
     float4 v[kPasses];
 };
 
@@ -106,12 +115,12 @@ template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     constexpr int kLds = DC + 4;     // padded LDS row (floats): conflict-free b128 reads
     using St = Stage<DC>;
-    __shared__ __attribute__((aligned(16))) float xs[2][kRows][kLds];
-    __shared__ float kb[kCSub][kQSub][16][64];
+    __shared__ __attribute__((aligned(16))) float xs[2][kSRows][kLds];
+    __shared__ float kb[kSCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
     __shared__ int64_t s_qid[kBM];
-    __shared__ float s_cn[2][kBN];
-    __shared__ int64_t s_cid[2][kBN];
+    __shared__ float s_cn[2][kSBN];
+    __shared__ int64_t s_cid[2][kSBN];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -125,7 +134,7 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     const int64_t q0 = (int64_t)qtile * kBM;
     const int64_t cb = (int64_t)split * p.cps;
     const int64_t ce = min(p.nc, cb + p.cps);
-    const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
+    const int64_t ntile = ce > cb ? (ce - cb + kSBN - 1) / kSBN : 0;
     const int nchunk = (int)((p.d + DC - 1) / DC);
     const int64_t total = ntile * nchunk;
     const int d = (int)p.d;
@@ -137,8 +146,8 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
         s_qid[tid] = (ok && p.qid) ? p.qid[q] : -1;
     }
     auto load_centre_meta = [&](int64_t tile) {
-        if (tid < kBN) {
-            const int64_t c = cb + tile * kBN + tid;
+        if (tid < kSBN) {
+            const int64_t c = cb + tile * kSBN + tid;
             const bool ok = c < ce;
             s_cn[tile & 1][tid] = ok ? p.cn[c] : 0.f;
             s_cid[tile & 1][tid] = ok ? (p.cid ? p.cid[c] : c) : -2;
@@ -188,7 +197,7 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     int64_t pf_tile = 0;                // next chunk to fetch
     int pf_ch = 0;
     auto fetch = [&](St& s) {
-        const int64_t c0 = cb + pf_tile * kBN;
+        const int64_t c0 = cb + pf_tile * kSBN;
         const __amdgpu_buffer_rsrc_t crs =
             make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
         const int kbase = pf_ch * DC;
@@ -245,7 +254,7 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     auto finish_chunk = [&]() {
         if (ch == nchunk - 1) {
             // epilogue: distances -> kernel values, stored in accumulator order
-            const int64_t c0 = cb + tile * kBN;
+            const int64_t c0 = cb + tile * kSBN;
             const int bl = qt_s * 32 + (lane & 31);
             const float qnb = s_qn[bl];
             const int64_t qidb = s_qid[bl];
@@ -269,15 +278,15 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
             // W fragments of the next step in flight during this step's MFMAs
             if (active) {
                 const __amdgpu_buffer_rsrc_t wrs =
-                    make_rsrc(p.W + c0 * p.ldw, (int64_t)kBN * p.ldw * 4);
+                    make_rsrc(p.W + c0 * p.ldw, (int64_t)kSBN * p.ldw * 4);
                 float acur[LTW], anxt[LTW];
                 load_w<LTW>(wrs, w_voff, w_soff(gj, 0), acur);
-                for (int jt = gj; jt < kCSub; jt += p.wj) {
+                for (int jt = gj; jt < kSCSub; jt += p.wj) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         if (v < 15)
                             load_w<LTW>(wrs, w_voff, w_soff(jt, v + 1), anxt);
-                        else if (jt + p.wj < kCSub)
+                        else if (jt + p.wj < kSCSub)
                             load_w<LTW>(wrs, w_voff, w_soff(jt + p.wj, 0), anxt);
                         const float k0v = kb[jt][0][v][lane];
                         const float k1v = kb[jt][1][v][lane];
@@ -343,35 +352,36 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
     }
 }
 
-// The same computation with the feature chunks copied from global memory
-// straight into LDS (buffer_load_dwordx4 ... lds: no staging registers) into
-// four rotating slots, issued three chunks ahead. Each wave reads its
-// operands one group (four MFMAs) ahead, also across the barrier that ends
-// a chunk (the next chunk's slot was published one barrier earlier), so its
-// MFMAs do not wait for LDS after a barrier. Requires the
-// VEC layout (d % 4 == 0, 16-byte aligned rows).
-template <int KIND, int LTW, bool ACC2>
-__device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
-    constexpr int DC = 32;                    // features per chunk (4 groups of 8)
-    constexpr int kSlot = kRows * DC;         // floats per slot (24 KB)
-    static_assert(kRows % 8 == 0 && kRows / 8 == 3 * (kThreads / 64), "3 loads per wave");
-    __shared__ __attribute__((aligned(16))) float xs0[kSlot];
-    __shared__ __attribute__((aligned(16))) float xs1[kSlot];
-    __shared__ __attribute__((aligned(16))) float xs2[kSlot];
-    __shared__ __attribute__((aligned(16))) float xs3[kSlot];
+// The same computation for rows that are 16-byte aligned (d % 4 == 0), with
+// 64 x 256 tiles. Each wave's 32 centre rows are read by that wave alone, so
+// they go from global memory straight into the MFMA A-operand registers (two
+// 16-byte loads per lane and chunk of 16 features), issued one batch of four
+// chunks ahead. Only the 64 query rows, which all eight waves read, pass
+// through LDS: a batch of 64 features is loaded into registers at the start
+// of the previous batch and written to one of two LDS buffers at its end, so
+// there is one workgroup barrier per batch instead of one per chunk. (Copying
+// both sides straight into shared LDS slots instead, with a barrier per
+// chunk, reached 77 % of the fp32 MFMA peak at 1000 labels against 85 % for
+// this form: the LDS slots cap the loads in flight, and the barriers stall
+// both waves of a SIMD at once.)
+constexpr int kRDC = 16;                 // features per chunk
+constexpr int kRB = 4;                   // chunks per batch
+constexpr int kRF = kRDC * kRB;          // features per batch (64)
+constexpr int kRQuads = kBM * kRF / 4;   // query quads per batch (1024)
+static_assert(kRQuads == 2 * kThreads, "two staged query quads per thread and batch");
+
+template <int KIND, int LTW>
+__device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
+    __shared__ __attribute__((aligned(16))) float qs[2][kBM * kRF];
     __shared__ float kb[kCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
     __shared__ int64_t s_qid[kBM];
     __shared__ float s_cn[2][kBN];
-    __shared__ int64_t s_cid[2][kBN];
+    __shared__ int64_t s_cid[2][kBN];     // only with explicit centre ids
+    __shared__ int s_qdiag[2][kBM];       // idem: tile position of the query's own centre
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    // wave index made visibly uniform: everything derived from it (label
-    // block, centre group, weight offsets) then lives in scalar registers,
-    // and buffer loads need no per-lane offset loops. Not for three label
-    // tiles per wave, whose three separate weight loads the scheduler then
-    // sinks next to their use (measured: a third slower).
     const int wave = LTW == 3 ? tid >> 6 : __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tq = (int)((p.nq + kBM - 1) / kBM);
@@ -381,8 +391,9 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
     const int64_t cb = (int64_t)split * p.cps;
     const int64_t ce = min(p.nc, cb + p.cps);
     const int64_t ntile = ce > cb ? (ce - cb + kBN - 1) / kBN : 0;
-    const int nchunk = (int)((p.d + DC - 1) / DC);
-    const int64_t total = ntile * nchunk;
+    const int nchunk = (int)((p.d + kRDC - 1) / kRDC);
+    const int nbt = (nchunk + kRB - 1) / kRB;            // batches per tile
+    const int64_t nbatch = ntile * nbt;
     const int d = (int)p.d;
 
     if (tid < kBM) {
@@ -396,18 +407,31 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
             const int64_t c = cb + tile * kBN + tid;
             const bool ok = c < ce;
             s_cn[tile & 1][tid] = ok ? p.cn[c] : 0.f;
-            s_cid[tile & 1][tid] = ok ? (p.cid ? p.cid[c] : c) : -2;
+            if (p.cid) s_cid[tile & 1][tid] = ok ? p.cid[c] : -2;
         }
     };
-    if (ntile > 0) load_centre_meta(0);
+    // With explicit centre ids (the subsample pass: centres are batch rows)
+    // the first wave finds, for each query, the tile position of the centre
+    // that is the same training point (ids are unique on both sides), after
+    // a barrier that publishes the tile's ids.
+    auto find_diag = [&](int64_t tile) {
+        if (tid < kBM) {
+            const int64_t id = s_qid[tid];
+            const int64_t* ids = s_cid[tile & 1];
+            int at = -1;
+#pragma unroll 8
+            for (int j = 0; j < kBN; ++j) at = ids[j] == id ? j : at;
+            s_qdiag[tile & 1][tid] = at;
+        }
+    };
 
-    const int qt_s = wave & 1;
-    const int ct_s = wave >> 1;
-    const int gl = wave % p.wl;
+    const int ct_s = wave;              // centre sub-tile of this wave (distances)
+    const int gl = wave % p.wl;         // contraction role of this wave
     const int gj = wave / p.wl;
     const int lb = gl * LTW * kTile;
     const int lvalid = p.lt * kTile;
     const bool active = wave < p.wl * p.wj && lb < lvalid;
+    const int h = lane >> 5;
 
     floatx16 facc[LTW][kQSub];
 #pragma unroll
@@ -416,132 +440,134 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
         for (int b = 0; b < kQSub; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
-    floatx16 sacc, sacc2;
+    floatx16 sacc[kQSub];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        sacc[v] = 0.f;
-        sacc2[v] = 0.f;
-    }
+    for (int b = 0; b < kQSub; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[b][v] = 0.f;
 
-    // Direct-to-LDS staging: load i (0..2) of this wave fills staged rows
-    // 8j .. 8j+7, j = 3*wave + i (query rows 0..63, then centre rows), one
-    // 16-byte quad per lane: lane L takes row 8j + L/8 and stores at quad
-    // position L%8, i.e. it fetches quad (L%8) ^ swz(row) of that row.
+    // Query staging: thread t moves quads t and t + 512 of the batch, i.e.
+    // row Q/16, features 4(Q%16) .. +3 of the batch's 64, to LDS position
+    // (Q%16) ^ (row%16) of its row (rows of 64 floats; the permutation puts
+    // the 16 rows that one b128 read serves on distinct banks).
     const int64_t q_rows = min((int64_t)kBM, p.nq - q0);
     const __amdgpu_buffer_rsrc_t qrs =
         make_rsrc(p.Q + q0 * p.ldq, ((q_rows - 1) * p.ldq + p.d) * 4);
-    int dma_voff[3], dma_col[3];
+    int qst_voff[2], qst_col[2], qst_lds[2];
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-        const int j = 3 * wv + i;
-        const int r = 8 * j + (lane >> 3);
-        const int q = (lane & 7) ^ swz32(r);
-        dma_col[i] = 4 * q;
-        dma_voff[i] = (r < kBM ? r * (int)p.ldq : (r - kBM) * (int)p.ldc) * 4 + 16 * q;
+    for (int i = 0; i < 2; ++i) {
+        const int Q = tid + kThreads * i;
+        const int row = Q >> 4, qq = Q & 15;
+        qst_col[i] = 4 * qq;
+        qst_voff[i] = row * (int)p.ldq * 4 + 16 * qq;
+        qst_lds[i] = row * kRF + ((qq ^ (row & 15)) << 2);
     }
-    int64_t pf_tile = 0;
-    int pf_ch = 0;
-    auto slot_of = [&](auto tag) -> float* {
-        constexpr int S = decltype(tag)::value;
-        if constexpr (S == 0) return xs0;
-        else if constexpr (S == 1) return xs1;
-        else if constexpr (S == 2) return xs2;
-        else return xs3;
-    };
-    auto dma = [&](auto tag) {
-        float* base = slot_of(tag);
-        const int64_t c0 = cb + pf_tile * kBN;
-        const __amdgpu_buffer_rsrc_t crs =
-            make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
-        const int kbase = pf_ch * DC;
+    // Every load is issued on every path (out-of-range ones at kOOB, which
+    // read zeros without touching memory), so that the number of loads in
+    // flight is the same on all paths and the compiler's wait counts stay
+    // exact instead of draining the queue.
+    float4 qstage[2];
+    auto qload = [&](int bi, bool valid) {
+        const int f0 = bi * kRF;
 #pragma unroll
-        for (int i = 0; i < 3; ++i) {
-            const int j = 3 * wv + i;
-            const int voff = kbase + dma_col[i] < d ? dma_voff[i] : kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(j < kBM / 8 ? qrs : crs,
-                                                     (lds_void*)(base + j * 8 * DC), 16, voff,
-                                                     kbase * 4, 0, 0);
+        for (int i = 0; i < 2; ++i) {
+            const int voff = valid && f0 + qst_col[i] < d ? qst_voff[i] : kOOB;
+            qstage[i] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(qrs, voff, f0 * 4, 0));
         }
-        if (++pf_ch == nchunk) {
-            pf_ch = 0;
-            ++pf_tile;
+    };
+    auto qwrite = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            *reinterpret_cast<float4*>(&qs[buf][qst_lds[i]]) = qstage[i];
+    };
+
+    // Centre operands: lane (row = lane%32, half h) of wave w feeds, for
+    // group g of a chunk, features 8g+4h .. 8g+4h+3 of centre 32w + lane%32
+    // (one 16-byte load); the query side uses the same map.
+    const int c_voff = ((ct_s * 32 + (lane & 31)) * (int)p.ldc + 4 * h) * 4;
+    float4 cring[kRB][2];
+#pragma unroll
+    for (int c = 0; c < kRB; ++c)
+        cring[c][0] = cring[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto centre_rsrc = [&](int64_t t) {
+        const int64_t c0 = cb + t * kBN;
+        return make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
+    };
+    auto cload = [&](__amdgpu_buffer_rsrc_t crs, int ch, bool valid, float4* dst) {
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            const int f0 = ch * kRDC + 8 * g;
+            const int voff = valid && f0 + 4 * h < d ? c_voff : kOOB;
+            dst[g] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, f0 * 4, 0));
         }
     };
 
-    // Operand reads: lane (row = lane%32, half h = lane/32) feeds features
-    // 8g+4h .. 8g+4h+3 of group g, as in the staged body.
-    const int h = lane >> 5;
-    const int f = (lane & 7) ^ ((lane >> 3) & 1);     // swz of rows at multiples of 16 + lane%32
-    const int a_off = (kBM + ct_s * 32 + (lane & 31)) * DC;
-    const int b_off = (qt_s * 32 + (lane & 31)) * DC;
-    auto rd = [&](const float* base, int off, int g) {
-        return *reinterpret_cast<const float4*>(base + off + (((2 * g + h) ^ f) << 2));
+    // B operand (queries) from LDS: quad 4c + 2g + h of row 32b + lane%32
+    const int q_base = (lane & 31) * kRF;
+    const int q_swz = (lane & 15) ^ h;
+    auto rdq = [&](int buf, int c, int g, int b) {
+        const int pos = ((4 * c + 2 * g) ^ q_swz) << 2;
+        return *reinterpret_cast<const float4*>(&qs[buf][q_base + b * 32 * kRF + pos]);
     };
-    auto mfma4 = [&](float4 a, float4 b) {
-        if (ACC2) {
-            sacc = mfma(a.x, b.x, sacc);
-            sacc2 = mfma(a.y, b.y, sacc2);
-            sacc = mfma(a.z, b.z, sacc);
-            sacc2 = mfma(a.w, b.w, sacc2);
-        } else {
-            sacc = mfma(a.x, b.x, sacc);
-            sacc = mfma(a.y, b.y, sacc);
-            sacc = mfma(a.z, b.z, sacc);
-            sacc = mfma(a.w, b.w, sacc);
-        }
+    float4 bring[2][kQSub];
+    auto mfma_group = [&](const float4& a, int e) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int b = 0; b < kQSub; ++b) sacc[b] = mfma(a[k], bring[e][b][k], sacc[b]);
     };
 
     const int w_col = lb + LTW * (lane & 31);
     const int ldw4 = (int)p.ldw * 4;
     const int w_voff = w_col < lvalid ? ((lane >> 5) << 2) * ldw4 + w_col * 4 : kOOB;
     auto w_soff = [&](int jt, int v) { return (jt * 32 + ((v >> 2) << 3) + (v & 3)) * ldw4; };
-
-    int64_t tile = 0;
-    int ch = 0;
-    float4 ra[2], rb[2];      // operand ring: group g in entry g % 2, read one group ahead
-    // Contraction weights in flight: PD k-steps ahead. With few labels per
-    // wave (LTW <= 2) a k-step is only 2*LTW MFMAs, too short to cover a
-    // global load, so all 16 fragments of a centre sub-tile are kept in
-    // flight, the first 16 issued during the tile's last chunk; with 3-4
-    // label tiles two k-steps ahead (measured: 1 -> 2 gains 1.5 points of
-    // peak at l = 1000, 4 no more).
     constexpr int PD = LTW <= 2 ? 16 : 2;
     float wbuf[PD][LTW];
     auto w_rsrc = [&](int64_t t) {
-        return make_rsrc(p.W + (cb + t * kBN) * p.ldw, (int64_t)kBN * p.ldw * 4);
+        const int64_t c0 = cb + t * kBN;
+        return make_rsrc(p.W + c0 * p.ldw, min((int64_t)kBN, ce - c0) * p.ldw * 4);
     };
-    auto finish_tile = [&]() {
+    // After the last batch of a tile: kernel values (in accumulator order,
+    // which is the operand order of the second product), then
+    // out^T[label, q] += W[c, label] * K[c, q] on the same MFMA.
+    auto finish_tile = [&](int64_t tile) {
         const int64_t c0 = cb + tile * kBN;
-        const int bl = qt_s * 32 + (lane & 31);
-        const float qnb = s_qn[bl];
-        const int64_t qidb = s_qid[bl];
         const float* cn = s_cn[tile & 1];
-        const int64_t* cid = s_cid[tile & 1];
+        const int cbase = ct_s * 32 + 4 * h;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int jl = ct_s * 32 + acc_row(v, lane);
-            const float dot = ACC2 ? sacc[v] + sacc2[v] : sacc[v];
-            float kv = kernel_value<KIND>(qnb + cn[jl] - 2.f * dot, p.scale);
-            if (qidb == cid[jl]) kv = 1.f;
-            if (c0 + jl >= ce) kv = 0.f;
-            kb[ct_s][qt_s][v][lane] = kv;
-            sacc[v] = 0.f;
-            sacc2[v] = 0.f;
+        for (int b = 0; b < kQSub; ++b) {
+            const int bl = b * 32 + (lane & 31);
+            const float qnb = s_qn[bl];
+            int dq;
+            if (p.cid) {
+                dq = s_qdiag[tile & 1][bl] - cbase;
+            } else {
+                const int64_t rel = s_qid[bl] - c0 - cbase;
+                dq = rel >= 0 && rel < 32 ? (int)rel : -1;
+            }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int jr = ((v >> 2) << 3) + (v & 3);
+                float kv = kernel_value<KIND>(qnb + cn[cbase + jr] - 2.f * sacc[b][v], p.scale);
+                if (dq == jr) kv = 1.f;
+                kb[ct_s][b][v][lane] = kv;
+            }
         }
         if (tile + 1 < ntile) load_centre_meta(tile + 1);
         wg_barrier<-1>();
+        if (p.cid && tile + 1 < ntile) find_diag(tile + 1);
         if (active) {
             const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
-            if constexpr (PD < 16)
 #pragma unroll
-                for (int v = 0; v < PD; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+            for (int v = 0; v < PD; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
             for (int jt = gj; jt < kCSub; jt += p.wj) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     float acur[LTW];
 #pragma unroll
                     for (int i = 0; i < LTW; ++i) acur[i] = wbuf[v % PD][i];
-                    // refill the entry with the fragment PD k-steps ahead
                     const int nv = v + PD < 16 ? v + PD : v + PD - 16;
                     const int njt = v + PD < 16 ? jt : jt + p.wj;
                     if (njt < kCSub) load_w<LTW>(wrs, w_voff, w_soff(njt, nv), wbuf[v % PD]);
@@ -555,71 +581,70 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
                 }
             }
         }
+#pragma unroll
+        for (int b = 0; b < kQSub; ++b)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sacc[b][v] = 0.f;
     };
 
-    // One chunk on slot S: its direct loads for chunk it+3 go to slot
-    // S+3 (mod 4), whose chunk (it-1) every wave finished reading before the
-    // previous barrier.
-    auto step = [&](auto tag, int64_t it) {
-        constexpr int S = decltype(tag)::value;
-        if (it + 3 < total) dma(std::integral_constant<int, (S + 3) & 3>{});
-        const float* cur = slot_of(tag);
-        const float* nxt = slot_of(std::integral_constant<int, (S + 1) & 3>{});
-        if constexpr (PD == 16) {
-            if (ch + 1 == nchunk && active) {
-                const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
+    if (ntile > 0) {
+        load_centre_meta(0);
+        if (p.cid) {
+            __syncthreads();
+            find_diag(0);
+        }
+        // batch 0: queries to LDS buffer 0, centres of tile 0 to the ring
+        qload(0, true);
+        const __amdgpu_buffer_rsrc_t crs0 = centre_rsrc(0);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
-            }
-        }
-        ra[1] = rd(cur, a_off, 1);
-        rb[1] = rd(cur, b_off, 1);
-        mfma4(ra[0], rb[0]);
-        ra[0] = rd(cur, a_off, 2);
-        rb[0] = rd(cur, b_off, 2);
-        mfma4(ra[1], rb[1]);
-        ra[1] = rd(cur, a_off, 3);
-        rb[1] = rd(cur, b_off, 3);
-        mfma4(ra[0], rb[0]);
-        // first group of chunk it+1, whichever tile it belongs to (after the
-        // last chunk this reads a stale slot, unused)
-        ra[0] = rd(nxt, a_off, 0);
-        rb[0] = rd(nxt, b_off, 0);
-        mfma4(ra[1], rb[1]);
-        // keep each group's reads ahead of the previous group's MFMAs (the
-        // scheduler would otherwise sink them to save eight registers)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // 2 LDS reads
-            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);   // 4 MFMAs
-        }
-        if (++ch == nchunk) {
-            finish_tile();
-            ++tile;
-            ch = 0;
-        }
-        // chunk it+2 (loaded one step ago) is complete in every wave and
-        // published; this chunk's slot is free for the next step's loads
-        if (it + 3 < total) wg_barrier<3>();
-        else wg_barrier<0>();
-    };
-
-    // prologue: chunks 0..2 into slots 0..2; 0 and 1 must be visible
-    if (total > 0) dma(std::integral_constant<int, 0>{});
-    if (total > 1) dma(std::integral_constant<int, 1>{});
-    if (total > 2) {
-        dma(std::integral_constant<int, 2>{});
-        wg_barrier<3>();
-    } else {
-        wg_barrier<0>();
+        for (int c = 0; c < kRB; ++c) cload(crs0, c, c < nchunk, cring[c]);
+        qwrite(0);
     }
-    ra[0] = rd(xs0, a_off, 0);
-    rb[0] = rd(xs0, b_off, 0);
-    for (int64_t it0 = 0; it0 < total; it0 += 4) {
-        step(std::integral_constant<int, 0>{}, it0);
-        if (it0 + 1 < total) step(std::integral_constant<int, 1>{}, it0 + 1);
-        if (it0 + 2 < total) step(std::integral_constant<int, 2>{}, it0 + 2);
-        if (it0 + 3 < total) step(std::integral_constant<int, 3>{}, it0 + 3);
+    wg_barrier<-1>();
+
+    // the batch after the current one, whose operands are fetched meanwhile
+    int64_t nx_tile = 0;
+    int nx_bi = 0;
+    auto advance = [&]() {
+        if (++nx_bi == nbt) {
+            nx_bi = 0;
+            ++nx_tile;
+        }
+    };
+    advance();
+    int64_t k = 0;
+    for (int64_t tile = 0; tile < ntile; ++tile) {
+        for (int bi = 0; bi < nbt; ++bi, ++k) {
+            const bool has_next = k + 1 < nbatch;
+            const int buf = (int)(k & 1);
+            const __amdgpu_buffer_rsrc_t crs_n = centre_rsrc(has_next ? nx_tile : tile);
+            qload(nx_bi, has_next);
+#pragma unroll
+            for (int b = 0; b < kQSub; ++b) bring[0][b] = rdq(buf, 0, 0, b);
+#pragma unroll
+            for (int c = 0; c < kRB; ++c) {
+                if (c == 0 || bi * kRB + c < nchunk) {
+#pragma unroll
+                    for (int b = 0; b < kQSub; ++b) bring[1][b] = rdq(buf, c, 1, b);
+                    mfma_group(cring[c][0], 0);
+                    // first group of the next chunk of this batch (stale
+                    // after the last, unused)
+#pragma unroll
+                    for (int b = 0; b < kQSub; ++b) bring[0][b] = rdq(buf, (c + 1) & (kRB - 1), 0, b);
+                    mfma_group(cring[c][1], 1);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+                }
+                // refill this ring entry with the same position of the next batch
+                cload(crs_n, nx_bi * kRB + c, has_next && nx_bi * kRB + c < nchunk, cring[c]);
+            }
+            qwrite(buf ^ 1);
+            wg_barrier<-1>();
+            advance();
+        }
+        finish_tile(tile);
     }
 
     if (active) {
@@ -643,12 +668,12 @@ __device__ __forceinline__ void kmv_body_dma(const KmvArgs& p) {
 // (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_dma<KIND, LTW, ACC2>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
 __global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_dma<KIND, LTW, ACC2>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 
