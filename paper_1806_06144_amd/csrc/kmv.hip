@@ -534,6 +534,15 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     // out^T[label, q] += W[c, label] * K[c, q] on the same MFMA.
     auto finish_tile = [&](int64_t tile) {
         const int64_t c0 = cb + tile * kBN;
+        // the first weight fragments travel while the kernel values are
+        // formed and published (not with four label tiles per wave, whose
+        // registers are full)
+        const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
+        auto first_weights = [&]() {
+#pragma unroll
+            for (int v = 0; v < PD; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+        };
+        if (LTW < 4 && active) first_weights();
         const float* cn = s_cn[tile & 1];
         const int cbase = ct_s * 32 + 4 * h;
 #pragma unroll
@@ -559,9 +568,7 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         wg_barrier<-1>();
         if (p.cid && tile + 1 < ntile) find_diag(tile + 1);
         if (active) {
-            const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
-#pragma unroll
-            for (int v = 0; v < PD; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+            if (LTW == 4) first_weights();
             for (int jt = gj; jt < kCSub; jt += p.wj) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {

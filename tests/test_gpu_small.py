@@ -73,6 +73,38 @@ def test_one_step_setup_predict(case):
     assert rel(P, P_o) < TOL_STEP
 
 
+EDGES = [
+    # n, d, kernel: feature counts around the 16-feature chunk and the
+    # 64-feature batch of the vector path (d % 4 == 0), one centre tile
+    # exactly full (256) or one centre past it
+    (700, 4, "gaussian"), (700, 12, "laplacian"), (700, 16, "gaussian"),
+    (700, 20, "laplacian"), (700, 44, "gaussian"), (700, 60, "laplacian"),
+    (700, 68, "gaussian"), (700, 128, "laplacian"), (700, 132, "gaussian"),
+    (700, 196, "laplacian"), (256, 64, "gaussian"), (257, 64, "laplacian"),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("n,d,kernel", EDGES, ids=[f"n{c[0]}-d{c[1]}-{c[2][:3]}" for c in EDGES])
+def test_feature_and_tile_edges(n, d, kernel):
+    l, s, k, m, bw = 5, 60, 4, 70, 1.3
+    X, Y, a0, rng = _problem(n, d, l, 5)
+    r = rng.choice(n, s, replace=False)
+    t = _batch(rng, n, r, m)
+    Z = (rng.standard_normal((40, d)) / np.sqrt(d)).astype(np.float32)
+    st = oracle.setup(X, kernel_id(kernel), bw, s, k, r)
+    a1_o, F_o = oracle.step(st, a0, t, Y[t])
+    with Gpu(X, l, kernel, bw, s, k, r) as g:
+        g.set_alpha(a0)
+        F = g.step(t, Y[t])
+        a1 = g.alpha()
+        P = g.predict(Z)
+    assert rel(F, F_o) < TOL_STEP
+    assert rel(a1 - a0, a1_o - a0) < TOL_STEP
+    # predictions checked on the GPU's own alpha (near-flat kernels cancel)
+    assert rel(P, oracle.predict(X, a1, Z, kernel_id(kernel), bw)) < TOL_STEP
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("kernel,k", [("gaussian", 12), ("laplacian", 0)])
 def test_epochs_from_zero(kernel, k):
