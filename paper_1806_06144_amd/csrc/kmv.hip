@@ -79,16 +79,18 @@ __device__ __forceinline__ float4 load_feat4(__amdgpu_buffer_rsrc_t r, int row_o
     return v;
 }
 
-// LTW consecutive weights (one per virtual label tile).
+// LTW consecutive weights (one per virtual label tile). Three come from one
+// 16-byte load whose fourth float (the next lane's first, or zero past the
+// descriptor) is dropped: one load instead of three.
 template <int LTW>
 __device__ __forceinline__ void load_w(__amdgpu_buffer_rsrc_t r, int voff, int soff, float* dst) {
-    if (LTW == 4) {
+    if constexpr (LTW >= 3) {
         const float4 v = __builtin_bit_cast(
             float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
         dst[0] = v.x;
         dst[1] = v.y;
         dst[2] = v.z;
-        dst[3] = v.w;
+        if constexpr (LTW == 4) dst[3] = v.w;
     } else if (LTW == 2) {
         const float2 v =
             __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
@@ -382,8 +384,10 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = LTW == 3 ? tid >> 6 : __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // wave index made visibly uniform: everything derived from it (label
+    // block, centre rows, weight offsets) then lives in scalar registers,
+    // and buffer loads need no per-lane offset loops
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tq = (int)((p.nq + kBM - 1) / kBM);
     const int split = (int)blockIdx.x / tq;
     const int qtile = (int)blockIdx.x - split * tq;
