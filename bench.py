@@ -335,7 +335,7 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="imagenet")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -420,10 +420,13 @@ def main():
         f"sigma_k+1={info.sigma_k1:.4f} eta={info.eta:.1f}")
 
     nb = args.warmup + args.steps
-    perm = synth.epoch_permutation(cfg.n, 0, 0)
-    batches = [perm[i * m:(i + 1) * m] for i in range(nb)]
-    if any(len(b) != m for b in batches):
-        raise SystemExit("not enough full batches in one epoch for the requested steps")
+    # full batches of successive epochs (the short last batch of each is
+    # timed on its own below)
+    batches, epoch = [], 0
+    while len(batches) < nb:
+        batches += [b for b in synth.epoch_batches(cfg.n, m, epoch) if len(b) == m]
+        epoch += 1
+    batches = batches[:nb]
     t_dev = [torch.from_numpy(b).to(dev) for b in batches]
     y_dev = [torch.from_numpy(synth.one_hot(labels[b], cfg.l)).to(dev) for b in batches]
 
@@ -431,15 +434,37 @@ def main():
         ep.ep_step(ctx, t_dev[i], m, y_dev[i])
     ep.ep_sync(ctx)
     ep.ep_timing_enable(ctx, True)
+    # the library works on torch's current stream here, so events recorded
+    # between its calls bracket each step on the GPU
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.warmup, nb):
+        evs[i - args.warmup].record(stream)
         ep.ep_step(ctx, t_dev[i], m, y_dev[i])
+    evs[-1].record(stream)
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     ep.ep_sync(ctx)
     tim = ep.ep_timing_read(ctx)
     ep.ep_timing_enable(ctx, False)
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+
+    # the short last batch of an epoch (n mod m rows), for the epoch time
+    last_ms = None
+    m_last = cfg.n % m
+    if m_last:
+        tl = synth.epoch_batches(cfg.n, m, 0)[-1]
+        tl_dev = torch.from_numpy(tl).to(dev)
+        yl_dev = torch.from_numpy(synth.one_hot(labels[tl], cfg.l)).to(dev)
+        ep.ep_step(ctx, tl_dev, m_last, yl_dev)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(3):
+            ep.ep_step(ctx, tl_dev, m_last, yl_dev)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        last_ms = ev0.elapsed_time(ev1) / 3
 
     # prediction (Section 2) of held-out rows with the trained alpha: the
     # same fused pass with m -> n_z, no diagonal rule
@@ -563,7 +588,10 @@ def main():
         "tflops_step2_pass": pass_tflops,
         "tflops_contraction_gemm": gemm_tflops,
         "tflops_whole_step": step_flops / sec_per_step / 1e12,
-        "s_per_epoch_est": (n / m) * sec_per_step,
+        "ms_per_step_median": float(np.median(step_ms)),
+        # floor(n/m) full steps at the median time plus the short last batch
+        "s_per_epoch": ((n // m) * float(np.median(step_ms)) + (last_ms or 0.0)) / 1e3,
+        "last_batch": {"m": int(m_last), "ms": last_ms},
         "setup_s": info.setup_ms / 1e3,
         "roofline": {
             "bound": "mfma",
