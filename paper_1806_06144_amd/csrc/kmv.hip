@@ -11,8 +11,8 @@
 //
 // One workgroup = 8 waves (two per SIMD) owns 64 query rows and a contiguous
 // range of centres (a "split"), walked 256 centres at a time:
-//   1. S = C_tile . Q_tile^T on fp32 MFMA (v_mfma_f32_32x32x2f32): each wave
-//      owns 32 centres x 64 queries (two 32x32 sub-tiles with independent
+//   1. S = C_tile . Q_tile^T on fp32 MFMA (v_mfma_f32_16x16x4f32): each wave
+//      owns 32 centres x 64 queries (2 x 4 blocks of 16 x 16 with independent
 //      accumulators) of the 256 x 64 block. Its centre rows, which no other
 //      wave reads, go from global memory straight into the MFMA operand
 //      registers one batch of 64 features ahead; the query rows, which all
@@ -42,6 +42,8 @@
 namespace ep {
 
 namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
 
@@ -358,7 +360,10 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
 // 64 x 256 tiles. Each wave's 32 centre rows are read by that wave alone, so
 // they go from global memory straight into the MFMA A-operand registers (two
 // 16-byte loads per lane and chunk of 16 features), issued one batch of four
-// chunks ahead. Only the 64 query rows, which all eight waves read, pass
+// chunks ahead. The distance product runs on the 16x16x4 MFMA, whose A
+// operand gives four lanes to a row: one load then covers 16 rows x 64
+// contiguous bytes (the 32x32x2 layout, two lanes per row, covers 32 rows x
+// 32 bytes and measured 1.8 % slower). Only the 64 query rows, which all eight waves read, pass
 // through LDS: a batch of 64 features is loaded into registers at the start
 // of the previous batch and written to one of two LDS buffers at its end, so
 // there is one workgroup barrier per batch instead of one per chunk. (Copying
@@ -435,7 +440,6 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     const int lb = gl * LTW * kTile;
     const int lvalid = p.lt * kTile;
     const bool active = wave < p.wl * p.wj && lb < lvalid;
-    const int h = lane >> 5;
 
     floatx16 facc[LTW][kQSub];
 #pragma unroll
@@ -444,11 +448,15 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         for (int b = 0; b < kQSub; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
-    floatx16 sacc[kQSub];
+    // distances: 2 centre blocks x 4 query blocks of 16 x 16 (16x16x4 MFMA)
+    floatx4 sacc[2][4];
 #pragma unroll
-    for (int b = 0; b < kQSub; ++b)
+    for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[b][v] = 0.f;
+        for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sacc[cb][qb][i] = 0.f;
+    const int q4 = lane >> 4;           // k slot of this lane in a 16x16x4 step
 
     // Query staging: thread t moves quads t and t + 512 of the batch, i.e.
     // row Q/16, features 4(Q%16) .. +3 of the batch's 64, to LDS position
@@ -486,10 +494,13 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
             *reinterpret_cast<float4*>(&qs[buf][qst_lds[i]]) = qstage[i];
     };
 
-    // Centre operands: lane (row = lane%32, half h) of wave w feeds, for
-    // group g of a chunk, features 8g+4h .. 8g+4h+3 of centre 32w + lane%32
-    // (one 16-byte load); the query side uses the same map.
-    const int c_voff = ((ct_s * 32 + (lane & 31)) * (int)p.ldc + 4 * h) * 4;
+    // Centre operands: lane (row = lane%16, k slot q4 = lane/16) of wave w
+    // feeds, for centre block cb, features 4q4 .. 4q4+3 of the chunk of
+    // centre 32w + 16cb + lane%16 (one 16-byte load); step i of the 16x16x4
+    // MFMA pairs feature 4q4 + i of both sides, so every feature is
+    // contracted exactly once.
+    const int c_voff = ((ct_s * 32 + (lane & 15)) * (int)p.ldc + 4 * q4) * 4;
+    const int c_blk = 16 * (int)p.ldc * 4;   // second centre block (soffset)
     float4 cring[kRB][2];
 #pragma unroll
     for (int c = 0; c < kRB; ++c)
@@ -499,28 +510,32 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         return make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
     };
     auto cload = [&](__amdgpu_buffer_rsrc_t crs, int ch, bool valid, float4* dst) {
+        const int f0 = ch * kRDC;
+        const int voff = valid && f0 + 4 * q4 < d ? c_voff : kOOB;
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            const int f0 = ch * kRDC + 8 * g;
-            const int voff = valid && f0 + 4 * h < d ? c_voff : kOOB;
-            dst[g] = __builtin_bit_cast(
-                float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, f0 * 4, 0));
-        }
+        for (int cb = 0; cb < 2; ++cb)
+            dst[cb] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, f0 * 4 + cb * c_blk, 0));
     };
 
     // B operand (queries) from LDS: quad 4c + 2g + h of row 32b + lane%32
-    const int q_base = (lane & 31) * kRF;
-    const int q_swz = (lane & 15) ^ h;
-    auto rdq = [&](int buf, int c, int g, int b) {
-        const int pos = ((4 * c + 2 * g) ^ q_swz) << 2;
-        return *reinterpret_cast<const float4*>(&qs[buf][q_base + b * 32 * kRF + pos]);
+    // B operand (queries) from LDS: quad 4c + q4 of row 16qb + lane%16
+    const int q_base = (lane & 15) * kRF;
+    const int q_swz = q4 ^ (lane & 15);
+    auto rdq = [&](int buf, int c, int qb) {
+        const int pos = ((4 * c) ^ q_swz) << 2;
+        return *reinterpret_cast<const float4*>(&qs[buf][q_base + qb * 16 * kRF + pos]);
     };
-    float4 bring[2][kQSub];
-    auto mfma_group = [&](const float4& a, int e) {
+    float4 bring[2][2];       // half e of a chunk: query blocks 2e, 2e+1
+    auto mfma_half = [&](const float4* a, int e) {
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
-            for (int b = 0; b < kQSub; ++b) sacc[b] = mfma(a[k], bring[e][b][k], sacc[b]);
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    sacc[cb][2 * e + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        a[cb][k], bring[e][j][k], sacc[cb][2 * e + j], 0, 0, 0);
     };
 
     const int w_col = lb + LTW * (lane & 31);
@@ -548,10 +563,12 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         };
         if (LTW < 4 && active) first_weights();
         const float* cn = s_cn[tile & 1];
-        const int cbase = ct_s * 32 + 4 * h;
+        // element i of block (cb, qb) is centre cbase + 16cb + i, query
+        // 16qb + lane%16; it goes where the 32x32 contraction reads it
+        const int cbase = ct_s * 32 + 4 * q4;
 #pragma unroll
-        for (int b = 0; b < kQSub; ++b) {
-            const int bl = b * 32 + (lane & 31);
+        for (int qb = 0; qb < 4; ++qb) {
+            const int bl = qb * 16 + (lane & 15);
             const float qnb = s_qn[bl];
             int dq;
             if (p.cid) {
@@ -560,13 +577,16 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
                 const int64_t rel = s_qid[bl] - c0 - cbase;
                 dq = rel >= 0 && rel < 32 ? (int)rel : -1;
             }
+            const int lk = 16 * (qb & 1) + (lane & 15) + 32 * (q4 & 1);
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int jr = ((v >> 2) << 3) + (v & 3);
-                float kv = kernel_value<KIND>(qnb + cn[cbase + jr] - 2.f * sacc[b][v], p.scale);
-                if (dq == jr) kv = 1.f;
-                kb[ct_s][b][v][lane] = kv;
-            }
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float kv = kernel_value<KIND>(qnb + cn[cbase + 16 * cb + i] - 2.f * sacc[cb][qb][i],
+                                                  p.scale);
+                    if (dq == 16 * cb + i) kv = 1.f;
+                    kb[ct_s][qb >> 1][8 * cb + 4 * (q4 >> 1) + i][lk] = kv;
+                }
         }
         if (tile + 1 < ntile) load_centre_meta(tile + 1);
         wg_barrier<-1>();
@@ -593,9 +613,11 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
             }
         }
 #pragma unroll
-        for (int b = 0; b < kQSub; ++b)
+        for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sacc[b][v] = 0.f;
+            for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sacc[cb][qb][i] = 0.f;
     };
 
     if (ntile > 0) {
@@ -631,22 +653,22 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
             const __amdgpu_buffer_rsrc_t crs_n = centre_rsrc(has_next ? nx_tile : tile);
             qload(nx_bi, has_next);
 #pragma unroll
-            for (int b = 0; b < kQSub; ++b) bring[0][b] = rdq(buf, 0, 0, b);
+            for (int j = 0; j < 2; ++j) bring[0][j] = rdq(buf, 0, j);
 #pragma unroll
             for (int c = 0; c < kRB; ++c) {
                 if (c == 0 || bi * kRB + c < nchunk) {
 #pragma unroll
-                    for (int b = 0; b < kQSub; ++b) bring[1][b] = rdq(buf, c, 1, b);
-                    mfma_group(cring[c][0], 0);
-                    // first group of the next chunk of this batch (stale
+                    for (int j = 0; j < 2; ++j) bring[1][j] = rdq(buf, c, 2 + j);
+                    mfma_half(cring[c], 0);
+                    // first half of the next chunk of this batch (stale
                     // after the last, unused)
 #pragma unroll
-                    for (int b = 0; b < kQSub; ++b) bring[0][b] = rdq(buf, (c + 1) & (kRB - 1), 0, b);
-                    mfma_group(cring[c][1], 1);
+                    for (int j = 0; j < 2; ++j) bring[0][j] = rdq(buf, (c + 1) & (kRB - 1), j);
+                    mfma_half(cring[c], 1);
                     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
                     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
                 }
                 // refill this ring entry with the same position of the next batch
                 cload(crs_n, nx_bi * kRB + c, has_next && nx_bi * kRB + c < nchunk, cring[c]);
