@@ -15,8 +15,8 @@
 //      owns 32 centres x 64 queries (2 x 4 blocks of 16 x 16 with independent
 //      accumulators) of the 256 x 64 block. Its centre rows, which no other
 //      wave reads, go from global memory straight into the MFMA operand
-//      registers one batch of 64 features ahead; the query rows, which all
-//      waves read, pass through LDS in batches of 64 features (double
+//      registers 64 features ahead; the query rows, which all waves read,
+//      pass through LDS in batches of 128 (or 64) features (double
 //      buffered, one barrier per batch). Rows that are not 16-byte aligned
 //      take a register-staged path with 128-centre tiles and LDS for both
 //      sides.
@@ -359,26 +359,38 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
 // The same computation for rows that are 16-byte aligned (d % 4 == 0), with
 // 64 x 256 tiles. Each wave's 32 centre rows are read by that wave alone, so
 // they go from global memory straight into the MFMA A-operand registers (two
-// 16-byte loads per lane and chunk of 16 features), issued one batch of four
-// chunks ahead. The distance product runs on the 16x16x4 MFMA, whose A
-// operand gives four lanes to a row: one load then covers 16 rows x 64
-// contiguous bytes (the 32x32x2 layout, two lanes per row, covers 32 rows x
-// 32 bytes and measured 1.8 % slower). Only the 64 query rows, which all eight waves read, pass
-// through LDS: a batch of 64 features is loaded into registers at the start
-// of the previous batch and written to one of two LDS buffers at its end, so
-// there is one workgroup barrier per batch instead of one per chunk. (Copying
-// both sides straight into shared LDS slots instead, with a barrier per
-// chunk, reached 77 % of the fp32 MFMA peak at 1000 labels against 85 % for
-// this form: the LDS slots cap the loads in flight, and the barriers stall
-// both waves of a SIMD at once.)
+// 16-byte loads per lane and chunk of 16 features), issued four chunks
+// ahead. The distance product runs on the 16x16x4 MFMA, whose A operand
+// gives four lanes to a row: one load then covers 16 rows x 64 contiguous
+// bytes (the 32x32x2 layout, two lanes per row, covers 32 rows x 32 bytes
+// and measured 1.8 % slower). Only the 64 query rows, which all eight waves
+// read, pass through LDS: each 64-feature part of a batch is loaded into
+// registers at the start of the previous part and written to one of two
+// LDS buffers at its end, so there is one workgroup barrier per batch (8 or
+// 4 chunks) instead of one per chunk. (Copying both sides straight into
+// shared LDS slots instead, with a barrier per chunk, reached 77 % of the
+// fp32 MFMA peak at 1000 labels against 89 % for this form: the LDS slots
+// cap the loads in flight, and the barriers stall both waves of a SIMD at
+// once.)
 constexpr int kRDC = 16;                 // features per chunk
-constexpr int kRB = 4;                   // chunks per batch
-constexpr int kRF = kRDC * kRB;          // features per batch (64)
-constexpr int kRQuads = kBM * kRF / 4;   // query quads per batch (1024)
-static_assert(kRQuads == 2 * kThreads, "two staged query quads per thread and batch");
+constexpr int kRP = 4;                   // chunks in flight in the centre ring
 
-template <int KIND, int LTW>
+// Chunks per batch (one barrier per batch): 8 when the feature count fills
+// them, else 4 (a last batch of 8 chunks half empty costs more than the
+// barriers it saves; at d = 440, 28 chunks, 2 %).
+inline int batch_chunks(int64_t d) {
+    const int64_t nchunk = (d + kRDC - 1) / kRDC;
+    return nchunk % 8 == 0 || nchunk % 8 > 4 ? 8 : 4;
+}
+
+template <int KIND, int LTW, int KRB>
 __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
+    constexpr int kRB = KRB;                 // chunks per batch
+    constexpr int kRF = kRDC * kRB;          // features per batch
+    constexpr int kQPR = kRF / 4;            // query quads per row and batch
+    constexpr int kRowStep = kThreads / kQPR;    // rows between a thread's quads
+    static_assert(kRB % kRP == 0, "the batch is staged in kRP-chunk parts");
+    static_assert(kBM * kQPR == 2 * kThreads * (kRB / kRP), "two quads per thread and part");
     __shared__ __attribute__((aligned(16))) float qs[2][kBM * kRF];
     __shared__ float kb[kCSub][kQSub][16][64];
     __shared__ float s_qn[kBM];
@@ -465,33 +477,31 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     const int64_t q_rows = min((int64_t)kBM, p.nq - q0);
     const __amdgpu_buffer_rsrc_t qrs =
         make_rsrc(p.Q + q0 * p.ldq, ((q_rows - 1) * p.ldq + p.d) * 4);
-    int qst_voff[2], qst_col[2], qst_lds[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int Q = tid + kThreads * i;
-        const int row = Q >> 4, qq = Q & 15;
-        qst_col[i] = 4 * qq;
-        qst_voff[i] = row * (int)p.ldq * 4 + 16 * qq;
-        qst_lds[i] = row * kRF + ((qq ^ (row & 15)) << 2);
-    }
+    // quads tid + 512 j: rows tid/kQPR + j kRowStep, the same quad of each
+    const int qst_row = tid / kQPR, qst_qq = tid % kQPR;
+    const int qst_col = 4 * qst_qq;
+    const int qst_voff = qst_row * (int)p.ldq * 4 + 16 * qst_qq;
+    const int qst_lds = qst_row * kRF + ((qst_qq ^ (qst_row & 15)) << 2);
+    const int qst_step = kRowStep * (int)p.ldq * 4;   // kRowStep rows further (soffset)
     // Every load is issued on every path (out-of-range ones at kOOB, which
     // read zeros without touching memory), so that the number of loads in
     // flight is the same on all paths and the compiler's wait counts stay
     // exact instead of draining the queue.
     float4 qstage[2];
-    auto qload = [&](int bi, bool valid) {
+    auto qload = [&](int part, int bi, bool valid) {
         const int f0 = bi * kRF;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int voff = valid && f0 + qst_col[i] < d ? qst_voff[i] : kOOB;
-            qstage[i] = __builtin_bit_cast(
-                float4, __builtin_amdgcn_raw_buffer_load_b128(qrs, voff, f0 * 4, 0));
-        }
-    };
-    auto qwrite = [&](int buf) {
+        const int voff = valid && f0 + qst_col < d ? qst_voff : kOOB;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-            *reinterpret_cast<float4*>(&qs[buf][qst_lds[i]]) = qstage[i];
+            qstage[i] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(
+                            qrs, voff, f0 * 4 + (2 * part + i) * qst_step, 0));
+    };
+    auto qwrite = [&](int part, int buf) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            *reinterpret_cast<float4*>(&qs[buf][qst_lds + (2 * part + i) * kRowStep * kRF]) =
+                qstage[i];
     };
 
     // Centre operands: lane (row = lane%16, k slot q4 = lane/16) of wave w
@@ -501,9 +511,9 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     // contracted exactly once.
     const int c_voff = ((ct_s * 32 + (lane & 15)) * (int)p.ldc + 4 * q4) * 4;
     const int c_blk = 16 * (int)p.ldc * 4;   // second centre block (soffset)
-    float4 cring[kRB][2];
+    float4 cring[kRP][2];
 #pragma unroll
-    for (int c = 0; c < kRB; ++c)
+    for (int c = 0; c < kRP; ++c)
         cring[c][0] = cring[c][1] = make_float4(0.f, 0.f, 0.f, 0.f);
     auto centre_rsrc = [&](int64_t t) {
         const int64_t c0 = cb + t * kBN;
@@ -626,12 +636,15 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
             __syncthreads();
             find_diag(0);
         }
-        // batch 0: queries to LDS buffer 0, centres of tile 0 to the ring
-        qload(0, true);
+        // batch 0: queries to LDS buffer 0, its first chunks to the ring
+#pragma unroll
+        for (int part = 0; part < kRB / kRP; ++part) {
+            qload(part, 0, true);
+            qwrite(part, 0);
+        }
         const __amdgpu_buffer_rsrc_t crs0 = centre_rsrc(0);
 #pragma unroll
-        for (int c = 0; c < kRB; ++c) cload(crs0, c, c < nchunk, cring[c]);
-        qwrite(0);
+        for (int c = 0; c < kRP; ++c) cload(crs0, c, c < nchunk, cring[c]);
     }
     wg_barrier<-1>();
 
@@ -650,30 +663,35 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         for (int bi = 0; bi < nbt; ++bi, ++k) {
             const bool has_next = k + 1 < nbatch;
             const int buf = (int)(k & 1);
+            const __amdgpu_buffer_rsrc_t crs_c = centre_rsrc(tile);
             const __amdgpu_buffer_rsrc_t crs_n = centre_rsrc(has_next ? nx_tile : tile);
-            qload(nx_bi, has_next);
 #pragma unroll
             for (int j = 0; j < 2; ++j) bring[0][j] = rdq(buf, 0, j);
 #pragma unroll
             for (int c = 0; c < kRB; ++c) {
+                if (c % kRP == 0) qload(c / kRP, nx_bi, has_next);
                 if (c == 0 || bi * kRB + c < nchunk) {
 #pragma unroll
                     for (int j = 0; j < 2; ++j) bring[1][j] = rdq(buf, c, 2 + j);
-                    mfma_half(cring[c], 0);
+                    mfma_half(cring[c % kRP], 0);
                     // first half of the next chunk of this batch (stale
                     // after the last, unused)
 #pragma unroll
                     for (int j = 0; j < 2; ++j) bring[0][j] = rdq(buf, (c + 1) & (kRB - 1), j);
-                    mfma_half(cring[c], 1);
+                    mfma_half(cring[c % kRP], 1);
                     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
                     __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
                     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
                     __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
                 }
-                // refill this ring entry with the same position of the next batch
-                cload(crs_n, nx_bi * kRB + c, has_next && nx_bi * kRB + c < nchunk, cring[c]);
+                // refill this ring entry with the chunk kRP positions on
+                if (c + kRP < kRB)
+                    cload(crs_c, bi * kRB + c + kRP, bi * kRB + c + kRP < nchunk, cring[c % kRP]);
+                else
+                    cload(crs_n, nx_bi * kRB + c + kRP - kRB,
+                          has_next && nx_bi * kRB + c + kRP - kRB < nchunk, cring[c % kRP]);
+                if (c % kRP == kRP - 1) qwrite(c / kRP, buf ^ 1);
             }
-            qwrite(buf ^ 1);
             wg_barrier<-1>();
             advance();
         }
@@ -699,32 +717,35 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
 
 // Two entry points with one body, so that profiles tell the predictions pass
 // (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
-template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
+// KRB: chunks per batch of the vector body (unused by the staged one).
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2, int KRB>
 __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_vec<KIND, LTW>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
-template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2>
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2, int KRB>
 __global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_vec<KIND, LTW>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 
 typedef void (*KmvFn)(KmvArgs);
 
-template <int KIND, bool VEC>
+template <int KIND, bool VEC, int KRB>
 KmvFn pick(int ltw, bool sub) {
     switch (ltw) {
-        case 1: return sub ? kmv_subsample_kernel<KIND, 1, VEC, 2, 32, true> : kmv_kernel<KIND, 1, VEC, 2, 32, true>;
-        case 2: return sub ? kmv_subsample_kernel<KIND, 2, VEC, 2, 64, true> : kmv_kernel<KIND, 2, VEC, 2, 64, true>;
-        case 3: return sub ? kmv_subsample_kernel<KIND, 3, VEC, 1, 64, false> : kmv_kernel<KIND, 3, VEC, 1, 64, false>;
-        default: return sub ? kmv_subsample_kernel<KIND, 4, VEC, 1, 32, false> : kmv_kernel<KIND, 4, VEC, 1, 32, false>;
+        case 1: return sub ? kmv_subsample_kernel<KIND, 1, VEC, 2, 32, true, KRB> : kmv_kernel<KIND, 1, VEC, 2, 32, true, KRB>;
+        case 2: return sub ? kmv_subsample_kernel<KIND, 2, VEC, 2, 64, true, KRB> : kmv_kernel<KIND, 2, VEC, 2, 64, true, KRB>;
+        case 3: return sub ? kmv_subsample_kernel<KIND, 3, VEC, 1, 64, false, KRB> : kmv_kernel<KIND, 3, VEC, 1, 64, false, KRB>;
+        default: return sub ? kmv_subsample_kernel<KIND, 4, VEC, 1, 32, false, KRB> : kmv_kernel<KIND, 4, VEC, 1, 32, false, KRB>;
     }
 }
 
-KmvFn kernel_for(int kind, int ltw, bool vec, bool sub) {
-    if (kind == 0) return vec ? pick<0, true>(ltw, sub) : pick<0, false>(ltw, sub);
-    return vec ? pick<1, true>(ltw, sub) : pick<1, false>(ltw, sub);
+// krb: chunks per batch of the vector body (batch_chunks), 4 or 8
+KmvFn kernel_for(int kind, int ltw, bool vec, bool sub, int krb) {
+    if (!vec) return kind == 0 ? pick<0, false, 4>(ltw, sub) : pick<1, false, 4>(ltw, sub);
+    if (kind == 0) return krb == 8 ? pick<0, true, 8>(ltw, sub) : pick<0, true, 4>(ltw, sub);
+    return krb == 8 ? pick<1, true, 8>(ltw, sub) : pick<1, true, 4>(ltw, sub);
 }
 
 int occupancy_slots(int kind, int ltw) {
@@ -738,7 +759,7 @@ int occupancy_slots(int kind, int ltw) {
             cus = prop.multiProcessorCount;
     }
     int per = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true, false),
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true, false, 8),
                                                      kThreads, 0) != hipSuccess ||
         per < 1)
         per = 1;
@@ -818,7 +839,8 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample
         b.W = a.W + (int64_t)t0 * kTile;
         b.out = a.out + (int64_t)t0 * kTile;
         b.lt = std::min(32, lt_total - t0);
-        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec, subsample), grid, dim3(kThreads), 0, s,
+        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec, subsample, batch_chunks(a.d)), grid,
+                           dim3(kThreads), 0, s,
                            b);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
