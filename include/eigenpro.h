@@ -272,9 +272,9 @@ int ep_timing_read(ep_ctx* ctx, ep_timing* out);
  *                        (at most block_bytes), then a GEMM adds block x
  *                        alpha chunk into F. Needs d % 4 == 0 and 16-byte aligned
  *                        rows (else the fused form runs).
- *   EP_CONTRACT_AUTO     the fused form (default). The blocked form takes
- *                        about as long at l = 1000 and is slower at small
- *                        l (its GEMM is skinny there), and it writes the
+ *   EP_CONTRACT_AUTO     the fused form (default). The blocked form is
+ *                        slower (a little at l = 1000, several times at
+ *                        small l, where its GEMM is skinny) and writes the
  *                        block to memory, so it is only taken on request.
  * Both forms give the same values up to float32 summation order. The
  * subsample pass of steps 4-5 always uses the fused form. */
