@@ -779,8 +779,9 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int
     KmvPlan best{};
     const int lt = (int)std::min<int64_t>(ldw / kTile, 32);
     // contraction layout (label groups wl x centre groups wj = 8 waves):
-    // fewest MFMA steps on the busiest wave, then fewest slices
-    const int layouts[3][2] = {{8, 1}, {4, 2}, {2, 4}};
+    // fewest MFMA steps on the busiest wave, then fewest slices (with one
+    // label tile, 1 x 8 keeps every wave busy)
+    const int layouts[4][2] = {{8, 1}, {4, 2}, {2, 4}, {1, 8}};
     int best_cost = 1 << 30;
     for (auto& lw : layouts) {
         const int wl = lw[0], wj = lw[1];
