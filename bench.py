@@ -268,7 +268,8 @@ def study_setup(args):
     return out
 
 
-def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note):
+def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note,
+                    out_path=os.path.join(ROOT, "profiles", "hbm_traffic.json")):
     """HBM bytes per launch of the dominant kernel from two rocprofv3 --pmc
     runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the
     same counter reads for the 1 GiB device copies of --calibrate-copy.
@@ -305,7 +306,7 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note
     f_kib, w_kib = np.mean(fe[kernel]), np.mean(wr[kernel])
     bytes_launch = (f_kib * rf + w_kib * wf) * 1024.0
     rec = {}
-    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    path = out_path
     try:
         with open(path) as f:
             rec = json.load(f)
