@@ -778,13 +778,16 @@ float kernel_scale(int kind, float bandwidth) {
 KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices) {
     KmvPlan best{};
     const int lt = (int)std::min<int64_t>(ldw / kTile, 32);
+    const int64_t nct = ceil_div(std::max<int64_t>(nc, 1), kBN);
     // contraction layout (label groups wl x centre groups wj = 8 waves):
     // fewest MFMA steps on the busiest wave, then fewest slices (with one
-    // label tile, 1 x 8 keeps every wave busy)
+    // label tile, 1 x 8 keeps every wave busy; not for short centre ranges,
+    // where its eight partial slices per split cost more than it saves)
     const int layouts[4][2] = {{8, 1}, {4, 2}, {2, 4}, {1, 8}};
     int best_cost = 1 << 30;
     for (auto& lw : layouts) {
         const int wl = lw[0], wj = lw[1];
+        if (wj == 8 && nct < 64) continue;
         const int ltw = (lt + wl - 1) / wl;
         if (ltw > kMaxLtw) continue;
         const int cost = ltw * (kCSub / wj);
@@ -797,7 +800,6 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int
     }
     const int slots = occupancy_slots(kind, best.ltw);
     const int64_t tq = ceil_div(std::max<int64_t>(nq, 1), kBM);
-    const int64_t nct = ceil_div(std::max<int64_t>(nc, 1), kBN);
     // splits of the centre axis: minimise the makespan of tq * splits equal
     // workgroups over the resident slots. A split's centre rows must stay
     // below the buffer-descriptor reach kOOB (loads at kOOB must fall
