@@ -807,22 +807,40 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int
     // max_slices asks for.
     const int64_t max_per = std::max<int64_t>(1, (int64_t)kOOB / (kBN * std::max<int64_t>(ldc, 1) * 4));
     const int64_t min_p = ceil_div(nct, max_per);
-    int64_t best_p = 1, best_per = nct;
-    double best_t = 1e300;
-    for (int64_t P = min_p; P <= nct && (P == min_p || P * best.wj <= max_slices); ++P) {
-        const int64_t per = ceil_div(nct, P);
-        const int64_t peff = ceil_div(nct, per);
-        if (peff != P || per > max_per) continue;
-        const int64_t rounds = ceil_div(tq * peff, slots);
-        const double t = (double)rounds * (double)(per + 1);
-        if (t < best_t) {
-            best_t = t;
-            best_p = peff;
-            best_per = per;
+    // Each workgroup is charged a fixed cost of `ovh` tiles on top of its
+    // tiles. The first pass charges one tile; the second charges what a
+    // workgroup's start-up (first operands in flight, partial sums written)
+    // costs against one tile's work, 128 / (d + l) tiles, and keeps at least
+    // four tiles per workgroup. Its choice is taken only when it is
+    // predicted to be more than 2 % faster (for instance 240 workgroups on
+    // 256 CUs become 3 full rounds).
+    auto choose = [&](double ovh, int64_t min_per, int64_t& bp, int64_t& bper) {
+        double bt = 1e300;
+        bp = 1;
+        bper = nct;
+        for (int64_t P = min_p; P <= nct && (P == min_p || P * best.wj <= max_slices); ++P) {
+            const int64_t per = ceil_div(nct, P);
+            const int64_t peff = ceil_div(nct, per);
+            if (peff != P || per > max_per || (P != min_p && per < min_per)) continue;
+            const int64_t rounds = ceil_div(tq * peff, slots);
+            const double t = (double)rounds * ((double)per + ovh);
+            if (t < bt) {
+                bt = t;
+                bp = peff;
+                bper = per;
+            }
         }
-    }
-    best.splits = (int)best_p;
-    best.cps = best_per * kBN;
+    };
+    auto cost = [&](int64_t P, int64_t per, double ovh) {
+        return (double)ceil_div(tq * P, slots) * ((double)per + ovh);
+    };
+    const double ovh = 128.0 / (double)(std::max<int64_t>(ldc, 1) + ldw);
+    int64_t p1, per1, p2, per2;
+    choose(1.0, 1, p1, per1);
+    choose(ovh, 4, p2, per2);
+    const bool second = cost(p2, per2, ovh) < 0.98 * cost(p1, per1, ovh);
+    best.splits = (int)(second ? p2 : p1);
+    best.cps = (second ? per2 : per1) * kBN;
     return best;
 }
 
