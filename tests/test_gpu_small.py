@@ -81,6 +81,8 @@ EDGES = [
     (700, 20, "laplacian"), (700, 44, "gaussian"), (700, 60, "laplacian"),
     (700, 68, "gaussian"), (700, 128, "laplacian"), (700, 132, "gaussian"),
     (700, 196, "laplacian"), (256, 64, "gaussian"), (257, 64, "laplacian"),
+    # long rows: 257 chunks (4-chunk batches) and 512 chunks (8-chunk)
+    (300, 4112, "gaussian"), (300, 8192, "laplacian"),
 ]
 
 
