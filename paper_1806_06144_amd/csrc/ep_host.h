@@ -21,7 +21,9 @@ int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
                               "%s: %s (%s)", #expr, hipGetErrorString(e_), __func__);  \
     } while (0)
 
-// Grow-only device buffer.
+// Grow-only device buffer. Growing frees the old allocation with hipFree,
+// which waits for all work on the device first, so kernels still queued
+// on the context stream never see their buffer released under them.
 struct DevBuf {
     void* p = nullptr;
     size_t bytes = 0;
