@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -38,11 +39,23 @@ KERNEL_SOURCES = {"kmv_kernel": ["kmv.hip", "ep_device.h"],
                   "kblock_kernel": ["kblock.hip", "ep_device.h"]}
 
 
+def code_text(src):
+    """C++ source with its comments removed and blank space collapsed, so
+    that a measurement stays attached to the code it measured when only
+    comments change (no string literal in the kernel sources holds a
+    comment marker)."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def kernel_source_sha(kernel="kmv_kernel"):
+    """sha256[:16] of the kernel's code (comments and blank space removed)."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_1806_06144_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_1806_06144_amd", "csrc", name)) as f:
+            h.update(code_text(f.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()[:16]
 
 
@@ -318,7 +331,7 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note
     with open(path, "w") as f:
         json.dump(rec, f, indent=1)
     lines = [f"workload: {workload}", f"kernel: {kernel}",
-             f"kernel source sha256[:16]: {kernel_source_sha(kernel)}", "",
+             f"kernel code sha256[:16] (comments removed): {kernel_source_sha(kernel)}", "",
              command_note, "",
              f"per-dispatch counter values (KiB; {kernel}: its first {n_step} dispatches, "
              "those of the warm-up and timed steps):"]

@@ -528,7 +528,6 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
                 float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, f0 * 4 + cb * c_blk, 0));
     };
 
-    // B operand (queries) from LDS: quad 4c + 2g + h of row 32b + lane%32
     // B operand (queries) from LDS: quad 4c + q4 of row 16qb + lane%16
     const int q_base = (lane & 15) * kRF;
     const int q_swz = q4 ^ (lane & 15);

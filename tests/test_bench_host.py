@@ -50,3 +50,12 @@ def test_traffic_summary_counts_only_the_step_dispatches(tmp_path):
     assert rec["bytes_per_launch"] == (1000.0 * 2 + 10.0) * 1024
     assert rec["source_sha"] == bench.kernel_source_sha("kmv_kernel")
     assert "its first 3 dispatches" in text
+
+
+def test_code_hash_ignores_comments_only():
+    src = "int f(int a) { // one\n  return a + 1; /* two\n lines */ }\n"
+    same = "int f(int a) {\n  // other words\n  return a + 1;\n}"
+    changed = "int f(int a) { return a + 2; }"
+    assert bench.code_text(src) == bench.code_text(same)
+    assert bench.code_text(src) != bench.code_text(changed)
+    assert "//" not in bench.code_text(src) and "/*" not in bench.code_text(src)

@@ -1,6 +1,6 @@
 """GPU vs fp64 oracle on small seeded problems that exercise the edges of
 the tiling: ragged query / centre / feature / label tails, label blocks
-above 1024, k = 0 (plain SGD), s = n, a single-point batch, a full batch,
+above 1024, label-tile counts that leave a wave's tiles partly empty, k = 0 (plain SGD), s = n, a single-point batch, a full batch,
 batch rows that are also subsample rows, and both kernels."""
 
 import numpy as np
@@ -18,6 +18,10 @@ CASES = [
     ("laplacian", 2000, 100, 160, 300, 40, 257, 2.0),
     ("gaussian", 600, 40, 1100, 64, 10, 70, 1.2),
     ("laplacian", 5000, 130, 7, 400, 60, 700, 3.0),
+    # 3 and 7 label tiles (2 x 4 wave layout with two and four tiles per
+    # wave, one of them partly empty)
+    ("laplacian", 3000, 48, 70, 300, 30, 200, 2.0),
+    ("gaussian", 2600, 96, 200, 256, 25, 300, 1.5),
 ]
 
 
