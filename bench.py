@@ -336,6 +336,8 @@ def traffic_summary(fetch_csv, write_csv, workload, kernel, n_step, command_note
              f"per-dispatch counter values (KiB; {kernel}: its first {n_step} dispatches, "
              "those of the warm-up and timed steps):"]
     for key in [kernel, "kmv_subsample_kernel", "copy"]:
+        if not fe.get(key) and not wr.get(key):
+            continue
         lines.append(f"  {key:21s} FETCH_SIZE " + ", ".join(f"{v:.6g}" for v in fe.get(key, [])))
         lines.append(f"  {key:21s} WRITE_SIZE " + ", ".join(f"{v:.6g}" for v in wr.get(key, [])))
     lines += ["", "calibration: a 1 GiB copy reads and writes 1048576 KiB;",
@@ -537,10 +539,14 @@ def main():
     n, d, l, s, k = cfg.n, cfg.d, cfg.l, cfg.s, cfg.k
     entries = m * n
     kmv_flops = 2.0 * m * n * (d + l)
-    step_flops = 2.0 * m * (n + s) * (d + l) + 4.0 * s * k * l
     kmv_avg_s = tim.kmv_ms / 1e3 / max(tim.kmv_launches, 1)
     pass_tflops = kmv_flops / kmv_avg_s / 1e12
     blocked = tim.kblock_launches > 0
+    # steps 4-5: the fused form keeps the kernel values of the subsample
+    # columns from step 2 and needs one s x m x l product; the blocked form
+    # recomputes them in a subsample pass (distances and product)
+    sub_flops = 2.0 * m * s * (d + l) if blocked else 2.0 * m * s * l
+    step_flops = kmv_flops + sub_flops + 4.0 * s * k * l
     if blocked:
         # dominant kernel: the kernel block (distances -> kernel values);
         # its algorithmic work is 2 d flops per entry, over all chunks

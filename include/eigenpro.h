@@ -174,7 +174,12 @@ int ep_restore(ep_ctx** ctx, const float* X, int64_t n, int64_t d, int64_t l,
  *   f_out   device float32 m x l or NULL: receives f(x_t) before the update.
  * Computes F = K(X_t, X) alpha, R = F - y_b, updates alpha_t -= c R and
  * alpha_r += c V D V^T K(X_r, X_t) R with D_i = (1 - sigma_{k+1}/sigma_i) /
- * sigma_i. Asynchronous. Indices outside [0, n) are not read or written
+ * sigma_i. K(X_r, X_t) is not recomputed: the fused step-2 pass keeps
+ * those columns of the kernel block (a context buffer of s x m floats, at
+ * most 2 GiB, grown on demand) as the paper reads them from its stored
+ * block; past that size, with the blocked form, or for rows that are not
+ * 16-byte aligned, a separate fused pass recomputes them.
+ * Asynchronous. Indices outside [0, n) are not read or written
  * and make the next ep_sync return EP_EINDEX; repeated indices are
  * rejected with EP_EINDEX only when index checking is enabled
  * (ep_set_checks), since that check copies t to the host and synchronises.
@@ -277,7 +282,8 @@ int ep_timing_read(ep_ctx* ctx, ep_timing* out);
  *                        small l, where its GEMM is skinny) and writes the
  *                        block to memory, so it is only taken on request.
  * Both forms give the same values up to float32 summation order. The
- * subsample pass of steps 4-5 always uses the fused form. */
+ * blocked form recomputes K(X_r, X_t) for steps 4-5 in a fused subsample
+ * pass (see ep_step). */
 enum { EP_CONTRACT_AUTO = 0, EP_CONTRACT_FUSED = 1, EP_CONTRACT_BLOCKED = 2 };
 /*   block_bytes  upper bound of the blocked form's kernel-block buffer
  *                (0: 2 GiB); chunks shrink to fit it, down to 256 centres.

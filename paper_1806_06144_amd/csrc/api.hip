@@ -68,6 +68,8 @@ struct ep_ctx {
     std::vector<unsigned char> seen;
 
     DevBuf norms, alpha, r_dev, Xs, xs_norms, V, Dk, err;
+    DevBuf kpos;                        // n ints: subsample position of each row, or -1
+    DevBuf ksb;                         // s x round_up(m, 64): K(X_r, X_t) captured in step 2
     // per-call scratch
     DevBuf xb, xb_norms, R, part, G, vt_part, W1, zn;
 
@@ -81,8 +83,8 @@ struct ep_ctx {
     DevBuf kbuf;                        // one centre chunk's kernel block
 
     ~ep_ctx() {
-        for (DevBuf* b : {&norms, &alpha, &r_dev, &Xs, &xs_norms, &V, &Dk, &err, &xb, &xb_norms,
-                          &R, &part, &G, &vt_part, &W1, &zn})
+        for (DevBuf* b : {&norms, &alpha, &r_dev, &Xs, &xs_norms, &V, &Dk, &err, &kpos, &ksb,
+                          &xb, &xb_norms, &R, &part, &G, &vt_part, &W1, &zn})
             b->release();
         for (auto& p : kmv_ev) {
             (void)hipEventDestroy(p.a);
@@ -100,6 +102,10 @@ struct ep_ctx {
 namespace {
 
 constexpr size_t kPartBudget = size_t(2) << 30;   // bytes of split partial sums
+// bytes of the captured subsample columns K(X_r, X_t); larger products run
+// the separate subsample pass (and the capture must stay below 2^31 bytes,
+// the reach of its buffer descriptor)
+constexpr size_t kKsbBudget = (size_t(2) << 30) - 256;
 
 int max_slices_for(int64_t rows_pad, int64_t ldw) {
     const size_t per = (size_t)rows_pad * (size_t)ldw * sizeof(float);
@@ -124,7 +130,7 @@ int record(hipStream_t s, std::vector<TimedPair>& v, bool start) {
 int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
             int64_t nq, const float* C, int64_t ldc, const float* cn, const int64_t* cid,
             int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed,
-            bool subsample) {
+            bool subsample, bool capture = false) {
     *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
     KmvPlan plan = kmv_plan(nq, nc, ldc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
     *slices = plan.slices();
@@ -148,6 +154,12 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
     a.out_rows = *rows_pad;
     a.kind = c->kind;
     a.scale = c->scale;
+    if (capture) {
+        a.kpos = c->kpos.as<int>();
+        a.ksb = c->ksb.as<float>();
+        a.ldk = *rows_pad;
+        a.s_rows = c->s;
+    }
     if (timed) {
         int rc = record(c->stream, c->kmv_ev, true);
         if (rc) return rc;
@@ -161,6 +173,19 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
 }
 
 constexpr size_t kKBlockBudget = size_t(2) << 30;   // bytes of one chunk's kernel block
+
+// rocBLAS handle of the context, bound to its stream.
+int ensure_blas(ep_ctx* c) {
+    if (!c->blas) {
+        if (rocblas_create_handle(&c->blas) != rocblas_status_success) {
+            c->blas = nullptr;
+            return fail(EP_EDEVICE, "rocblas_create_handle failed");
+        }
+    }
+    if (rocblas_set_stream(c->blas, c->stream) != rocblas_status_success)
+        return fail(EP_EDEVICE, "rocblas_set_stream failed");
+    return EP_OK;
+}
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -188,13 +213,7 @@ int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const i
     int64_t ldo = (int64_t)(c->block_bytes / ((size_t)rows256 * sizeof(float))) / 256 * 256;
     ldo = std::max<int64_t>(256, std::min<int64_t>(ldo, round_up(c->n, 256)));
     HIP_TRY(c->kbuf.ensure((size_t)rows256 * ldo * sizeof(float)));
-    if (!c->blas) {
-        if (rocblas_create_handle(&c->blas) != rocblas_status_success) {
-            c->blas = nullptr;
-            return fail(EP_EDEVICE, "rocblas_create_handle failed");
-        }
-    }
-    rocblas_set_stream(c->blas, st);
+    if (int rc = ensure_blas(c)) return rc;
     const size_t slice_elems = (size_t)(*rows_pad) * c->l_pad;
     int rc = EP_OK;
     int64_t sub = 0;
@@ -241,12 +260,22 @@ int run_blocked(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const i
 }
 
 // F = K(Q, X) alpha over all training points: blocked or fused form.
+// With `capture` (fused form only) the pass also stores the kernel values of
+// the subsample columns, K(X_r, X_t), in c->ksb.
 int run_main_pass(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64_t* qid,
-                  int64_t nq, int* slices, int64_t* rows_pad, bool timed) {
+                  int64_t nq, int* slices, int64_t* rows_pad, bool timed, bool capture = false) {
     if (use_blocked(c, Q, ldq))
         return run_blocked(c, Q, ldq, qn, qid, nq, slices, rows_pad, timed);
     return run_kmv(c, Q, ldq, qn, qid, nq, c->X, c->d, c->norms.as<float>(), nullptr, c->n,
-                   c->alpha.as<float>(), slices, rows_pad, timed, false);
+                   c->alpha.as<float>(), slices, rows_pad, timed, false, capture);
+}
+
+// Whether step 2 of a batch of m rows (gathered, row length d) captures the
+// subsample columns for steps 4-5: fused form, vector body, and a capture
+// buffer within budget.
+bool capture_subsample(const ep_ctx* c, const float* xb, int64_t m) {
+    return c->k > 0 && !use_blocked(c, xb, c->d) && kmv_vec(xb, c->d, c->X, c->d, c->d) &&
+           (size_t)c->s * (size_t)round_up(m, kBM) * sizeof(float) <= kKsbBudget;
 }
 
 struct DeviceGuard {
@@ -513,6 +542,15 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sig
     HIP_TRY(launch_fill_f32(c->norms.as<float>(), c->n_pad, 0.f, st));
     HIP_TRY(hipMemcpyAsync(c->r_dev.p, c->r_host.data(), s * sizeof(int64_t),
                            hipMemcpyHostToDevice, st));
+    {
+        // subsample position of every training row (-1: not in r), which
+        // lets step 2 keep the kernel values of the subsample columns
+        std::vector<int32_t> kp((size_t)n, -1);
+        for (int64_t i = 0; i < s; ++i) kp[(size_t)c->r_host[i]] = (int32_t)i;
+        HIP_TRY(c->kpos.ensure((size_t)n * sizeof(int32_t)));
+        HIP_TRY(hipMemcpy(c->kpos.p, kp.data(), (size_t)n * sizeof(int32_t),
+                          hipMemcpyHostToDevice));
+    }
     HIP_TRY(launch_row_norms(c->X, n, d, d, c->norms.as<float>(), st));
     HIP_TRY(launch_gather_rows(c->X, n, d, c->norms.as<float>(), c->r_dev.as<int64_t>(), s,
                                c->s_pad, c->Xs.as<float>(), c->xs_norms.as<float>(),
@@ -673,10 +711,13 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     // step 1: gather the batch
     HIP_TRY(launch_gather_rows(c->X, c->n, c->d, c->norms.as<float>(), t, m, m_pad, xb, xbn,
                                c->err.as<int>(), st));
-    // step 2: F = K(X_t, X) alpha, fused
+    // step 2: F = K(X_t, X) alpha, fused; the kernel values of the
+    // subsample columns are kept for steps 4-5 when the buffer allows
     int slices = 0;
     int64_t rows_pad = 0;
-    rc = run_main_pass(c, xb, c->d, xbn, t, m, &slices, &rows_pad, c->timing);
+    const bool capture = capture_subsample(c, xb, m);
+    if (capture) HIP_TRY(c->ksb.ensure((size_t)c->s * round_up(m, kBM) * sizeof(float)));
+    rc = run_main_pass(c, xb, c->d, xbn, t, m, &slices, &rows_pad, c->timing, capture);
     if (rc) return rc;
     // step 3: R = F - y_b; alpha_t -= c R
     const double coef = 1.0 / (c->info.beta + (double)(m - 1) * c->info.lambda_k1);
@@ -684,12 +725,27 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
                                    f_out, R, m_pad, alpha, c->n, t, (float)coef, st));
     if (c->k > 0) {
         // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
-        rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(), c->r_dev.as<int64_t>(),
-                     c->s, xb, c->d, xbn, t, m, R, &slices, &rows_pad, false, true);
-        if (rc) return rc;
         HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
-        HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s, c->l_pad,
-                                   c->G.as<float>(), c->l_pad, st));
+        if (capture) {
+            // from the captured columns: G^T = R^T K(X_r, X_t)^T, one GEMM
+            // (column-major view: R^T is l_pad x m, ksb holds K^T as m x s)
+            if ((rc = ensure_blas(c))) return rc;
+            const float one = 1.f, zero = 0.f;
+            const rocblas_status gs = rocblas_sgemm(
+                c->blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)c->l_pad,
+                (rocblas_int)c->s, (rocblas_int)m, &one, R, (rocblas_int)c->l_pad,
+                c->ksb.as<float>(), (rocblas_int)rows_pad, &zero, c->G.as<float>(),
+                (rocblas_int)c->l_pad);
+            if (gs != rocblas_status_success)
+                return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        } else {
+            rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(),
+                         c->r_dev.as<int64_t>(), c->s, xb, c->d, xbn, t, m, R, &slices,
+                         &rows_pad, false, true);
+            if (rc) return rc;
+            HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s,
+                                       c->l_pad, c->G.as<float>(), c->l_pad, st));
+        }
         const int64_t per_slice = ceil_div(c->l_pad, 64) * ceil_div(c->k, 64);
         const int vs = (int)std::max<int64_t>(
             1, std::min<int64_t>(512 / std::max<int64_t>(per_slice, 1), ceil_div(c->s, 64)));

@@ -43,6 +43,14 @@ struct KmvArgs {
     int wl, wj;            // contraction layout: label groups x centre groups
     int kind;              // EP_GAUSSIAN / EP_LAPLACIAN
     float scale;           // exp2 argument scale (see kmv.hip)
+    // Optional (vector body only): kpos[j] >= 0 marks centre j as a
+    // subsample row; its kernel values k(q_i, c_j) are then also stored at
+    // ksb[kpos[j] * ldk + i] (ldk >= nq rounded up to kBM, kpos[j] <
+    // s_rows). NULL: none.
+    const int* kpos;
+    float* ksb;
+    int64_t ldk;
+    int64_t s_rows;        // rows of ksb; s_rows * ldk * 4 < 2^31
 };
 
 // Chooses splits / wave layout and launches; returns the number of partial
@@ -56,9 +64,17 @@ struct KmvPlan {
     int slices() const { return splits * wj; }
 };
 KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices);
-// Launches one fused pass per block of up to 1024 label columns. `subsample`
-// selects the entry point used for the subsample pass (same code, its own
-// symbol in profiles).
+// Whether a fused launch takes the vector body: d % 4 == 0 and every query
+// and centre row 16-byte aligned (the staged body serves the rest).
+inline bool kmv_vec(const float* Q, int64_t ldq, const float* C, int64_t ldc, int64_t d) {
+    return d % 4 == 0 && (ldq & 3) == 0 && (ldc & 3) == 0 &&
+           (reinterpret_cast<uintptr_t>(Q) & 15) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+}
+// Launches one fused pass per block of up to 1024 label columns (kernel
+// values are captured into ksb by the first only). `subsample` selects the
+// entry point used for the subsample pass (same code, its own symbol in
+// profiles). Capturing (kpos) needs the vector body: hipErrorInvalidValue
+// otherwise.
 hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample);
 
 float kernel_scale(int kind, float bandwidth);

@@ -398,6 +398,7 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     __shared__ float s_cn[2][kBN];
     __shared__ int64_t s_cid[2][kBN];     // only with explicit centre ids
     __shared__ int s_qdiag[2][kBM];       // idem: tile position of the query's own centre
+    __shared__ int s_cpos[2][kBN];        // only with kpos: subsample position or -1
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -429,6 +430,7 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
             const bool ok = c < ce;
             s_cn[tile & 1][tid] = ok ? p.cn[c] : 0.f;
             if (p.cid) s_cid[tile & 1][tid] = ok ? p.cid[c] : -2;
+            if (p.kpos) s_cpos[tile & 1][tid] = ok ? p.kpos[c] : -1;
         }
     };
     // With explicit centre ids (the subsample pass: centres are batch rows)
@@ -596,6 +598,28 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
                     if (dq == 16 * cb + i) kv = 1.f;
                     kb[ct_s][qb >> 1][8 * cb + 4 * (q4 >> 1) + i][lk] = kv;
                 }
+        }
+        // Subsample centres (kpos >= 0): their kernel values also go to row
+        // kpos of ksb, for the subsample correction. Each wave copies its
+        // own 32 centres back from its block of kb, one 64-query column per
+        // flagged centre (centre r of the block, query q sits at
+        // kb[.][q / 32][4 (r / 8) + r % 4][q % 32 + 32 ((r / 4) % 2)]).
+        if (p.kpos) {
+            const int* cp = s_cpos[tile & 1] + ct_s * 32;
+            uint64_t flagged = __ballot(lane < 32 && cp[lane & 31] >= 0);
+            if (flagged) {
+                const __amdgpu_buffer_rsrc_t ks = make_rsrc(p.ksb, (int64_t)p.s_rows * p.ldk * 4);
+                const float* kcol = &kb[ct_s][lane >> 5][0][lane & 31];
+                do {
+                    const int r = __builtin_ctzll(flagged);
+                    flagged &= flagged - 1;
+                    const int pos = __builtin_amdgcn_readfirstlane(cp[r]);
+                    const float v = kcol[(4 * (r >> 3) + (r & 3)) * 64 + 32 * ((r >> 2) & 1)];
+                    // (the store takes its data as 32 raw bits)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ks,
+                                                          lane * 4, (int)((pos * p.ldk + q0) * 4), 0);
+                } while (flagged);
+            }
         }
         if (tile + 1 < ntile) load_centre_meta(tile + 1);
         wg_barrier<-1>();
@@ -848,9 +872,8 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample
     a.splits = p.splits;
     a.wl = p.wl;
     a.wj = p.wj;
-    const bool vec = (a.d % 4 == 0) && ((a.ldq & 3) == 0) && ((a.ldc & 3) == 0) &&
-                     ((reinterpret_cast<uintptr_t>(a.Q) & 15) == 0) &&
-                     ((reinterpret_cast<uintptr_t>(a.C) & 15) == 0);
+    const bool vec = kmv_vec(a.Q, a.ldq, a.C, a.ldc, a.d);
+    if (a.kpos && !vec) return hipErrorInvalidValue;
     const int64_t tq = ceil_div(std::max<int64_t>(a.nq, 1), kBM);
     dim3 grid((unsigned)(tq * p.splits));
     const int lt_total = a.lt;
@@ -859,6 +882,7 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample
         b.W = a.W + (int64_t)t0 * kTile;
         b.out = a.out + (int64_t)t0 * kTile;
         b.lt = std::min(32, lt_total - t0);
+        if (t0 > 0) b.kpos = nullptr;
         hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec, subsample, batch_chunks(a.d)), grid,
                            dim3(kThreads), 0, s,
                            b);
