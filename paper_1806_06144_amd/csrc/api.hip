@@ -106,6 +106,7 @@ constexpr size_t kPartBudget = size_t(2) << 30;   // bytes of split partial sums
 // the separate subsample pass (and the capture must stay below 2^31 bytes,
 // the reach of its buffer descriptor)
 constexpr size_t kKsbBudget = (size_t(2) << 30) - 256;
+constexpr int64_t kGChunk = 512;   // batch rows per GEMM of steps 4-5
 
 int max_slices_for(int64_t rows_pad, int64_t ldw) {
     const size_t per = (size_t)rows_pad * (size_t)ldw * sizeof(float);
@@ -727,17 +728,24 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
         // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
         HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
         if (capture) {
-            // from the captured columns: G^T = R^T K(X_r, X_t)^T, one GEMM
-            // (column-major view: R^T is l_pad x m, ksb holds K^T as m x s)
+            // from the captured columns: G^T = R^T K(X_r, X_t)^T (column-major
+            // view: R^T is l_pad x m, ksb holds K^T as m x s), in chunks of
+            // kGChunk batch rows accumulated into G: a library GEMM sums its
+            // whole depth in one float32 chain, so the depth is split as the
+            // subsample pass splits its centres
             if ((rc = ensure_blas(c))) return rc;
-            const float one = 1.f, zero = 0.f;
-            const rocblas_status gs = rocblas_sgemm(
-                c->blas, rocblas_operation_none, rocblas_operation_none, (rocblas_int)c->l_pad,
-                (rocblas_int)c->s, (rocblas_int)m, &one, R, (rocblas_int)c->l_pad,
-                c->ksb.as<float>(), (rocblas_int)rows_pad, &zero, c->G.as<float>(),
-                (rocblas_int)c->l_pad);
-            if (gs != rocblas_status_success)
-                return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+            const float one = 1.f;
+            for (int64_t b0 = 0; b0 < m; b0 += kGChunk) {
+                const int64_t kk = std::min<int64_t>(kGChunk, m - b0);
+                const float beta = b0 == 0 ? 0.f : 1.f;
+                const rocblas_status gs = rocblas_sgemm(
+                    c->blas, rocblas_operation_none, rocblas_operation_none,
+                    (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)kk, &one,
+                    R + b0 * c->l_pad, (rocblas_int)c->l_pad, c->ksb.as<float>() + b0,
+                    (rocblas_int)rows_pad, &beta, c->G.as<float>(), (rocblas_int)c->l_pad);
+                if (gs != rocblas_status_success)
+                    return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+            }
         } else {
             rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(),
                          c->r_dev.as<int64_t>(), c->s, xb, c->d, xbn, t, m, R, &slices,
