@@ -107,6 +107,10 @@ constexpr size_t kPartBudget = size_t(2) << 30;   // bytes of split partial sums
 // the reach of its buffer descriptor)
 constexpr size_t kKsbBudget = (size_t(2) << 30) - 256;
 constexpr int64_t kGChunk = 512;   // batch rows per GEMM of steps 4-5
+// subsample rows per partial product V^T G: the top eigenvector's component
+// of G sums terms that largely cancel, and predictions scale its rounding
+// error by the kernel's largest eigenvalue, so its sums are kept short
+constexpr int64_t kVChunk = 64;
 
 int max_slices_for(int64_t rows_pad, int64_t ldw) {
     const size_t per = (size_t)rows_pad * (size_t)ldw * sizeof(float);
@@ -272,11 +276,13 @@ int run_main_pass(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const
 }
 
 // Whether step 2 of a batch of m rows (gathered, row length d) captures the
-// subsample columns for steps 4-5: fused form, vector body, and a capture
-// buffer within budget.
+// subsample columns for steps 4-5: fused form, vector body, and the capture
+// buffer and the product's partial slices within budget.
 bool capture_subsample(const ep_ctx* c, const float* xb, int64_t m) {
+    const size_t g_slices = (size_t)ceil_div(m, kGChunk) * c->s * c->l_pad * sizeof(float);
     return c->k > 0 && !use_blocked(c, xb, c->d) && kmv_vec(xb, c->d, c->X, c->d, c->d) &&
-           (size_t)c->s * (size_t)round_up(m, kBM) * sizeof(float) <= kKsbBudget;
+           (size_t)c->s * (size_t)round_up(m, kBM) * sizeof(float) <= kKsbBudget &&
+           g_slices <= kPartBudget;
 }
 
 struct DeviceGuard {
@@ -729,23 +735,41 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
         HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
         if (capture) {
             // from the captured columns: G^T = R^T K(X_r, X_t)^T (column-major
-            // view: R^T is l_pad x m, ksb holds K^T as m x s), in chunks of
-            // kGChunk batch rows accumulated into G: a library GEMM sums its
-            // whole depth in one float32 chain, so the depth is split as the
-            // subsample pass splits its centres
+            // view: R^T is l_pad x m, ksb holds K^T as m x s), split over
+            // the batch into chunks of kGChunk rows with one partial slice
+            // each (strided-batched, so the chunks' tiles fill the chip
+            // together), then summed: a library GEMM sums its whole depth in
+            // one float32 chain, so the depth is kept short as the
+            // subsample pass keeps its centre splits short
             if ((rc = ensure_blas(c))) return rc;
-            const float one = 1.f;
-            for (int64_t b0 = 0; b0 < m; b0 += kGChunk) {
-                const int64_t kk = std::min<int64_t>(kGChunk, m - b0);
-                const float beta = b0 == 0 ? 0.f : 1.f;
-                const rocblas_status gs = rocblas_sgemm(
-                    c->blas, rocblas_operation_none, rocblas_operation_none,
-                    (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)kk, &one,
-                    R + b0 * c->l_pad, (rocblas_int)c->l_pad, c->ksb.as<float>() + b0,
-                    (rocblas_int)rows_pad, &beta, c->G.as<float>(), (rocblas_int)c->l_pad);
-                if (gs != rocblas_status_success)
-                    return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+            const int64_t full = m / kGChunk, tail = m - full * kGChunk;
+            const int64_t nsl = full + (tail > 0 ? 1 : 0);
+            const size_t slice = (size_t)c->s * c->l_pad;
+            float* dst = nsl == 1 ? c->G.as<float>() : nullptr;
+            if (nsl > 1) {
+                HIP_TRY(c->part.ensure((size_t)nsl * slice * sizeof(float)));
+                dst = c->part.as<float>();
             }
+            const float one = 1.f, zero = 0.f;
+            rocblas_status gs = rocblas_status_success;
+            if (full > 0)
+                gs = rocblas_sgemm_strided_batched(
+                    c->blas, rocblas_operation_none, rocblas_operation_none,
+                    (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)kGChunk, &one, R,
+                    (rocblas_int)c->l_pad, (rocblas_stride)(kGChunk * c->l_pad),
+                    c->ksb.as<float>(), (rocblas_int)rows_pad, (rocblas_stride)kGChunk, &zero,
+                    dst, (rocblas_int)c->l_pad, (rocblas_stride)slice, (rocblas_int)full);
+            if (gs == rocblas_status_success && tail > 0)
+                gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_none,
+                                   (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)tail,
+                                   &one, R + full * kGChunk * c->l_pad, (rocblas_int)c->l_pad,
+                                   c->ksb.as<float>() + full * kGChunk, (rocblas_int)rows_pad,
+                                   &zero, dst + full * slice, (rocblas_int)c->l_pad);
+            if (gs != rocblas_status_success)
+                return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+            if (nsl > 1)
+                HIP_TRY(launch_reduce_rows(c->part.as<float>(), (int)nsl, c->s, c->l_pad, c->s,
+                                           c->l_pad, c->G.as<float>(), c->l_pad, st));
         } else {
             rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(),
                          c->r_dev.as<int64_t>(), c->s, xb, c->d, xbn, t, m, R, &slices,
@@ -754,18 +778,49 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
             HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s,
                                        c->l_pad, c->G.as<float>(), c->l_pad, st));
         }
-        const int64_t per_slice = ceil_div(c->l_pad, 64) * ceil_div(c->k, 64);
-        const int vs = (int)std::max<int64_t>(
-            1, std::min<int64_t>(512 / std::max<int64_t>(per_slice, 1), ceil_div(c->s, 64)));
-        HIP_TRY(c->vt_part.ensure((size_t)vs * round_up(c->k, 64) * c->l_pad * sizeof(float)));
+        // W = D V^T G: partial products over kVChunk-row chunks of the
+        // subsample (strided-batched; column-major view: slice j is
+        // G_j^T V_j, G_j^T l_pad x kVChunk, V_j^T k_ld x kVChunk), summed
+        // and scaled by D; then H = V W on the matrix cores (H^T = W^T V^T,
+        // depth k) into G's buffer, which W no longer needs, and
+        // alpha_r += c H
+        if ((rc = ensure_blas(c))) return rc;
+        const int64_t k_pad = round_up(c->k, 64);
+        const int64_t sfull = c->s / kVChunk, stail = c->s - sfull * kVChunk;
+        const int64_t nvs = sfull + (stail > 0 ? 1 : 0);
+        const size_t vslice = (size_t)k_pad * c->l_pad;
+        HIP_TRY(c->vt_part.ensure((size_t)nvs * vslice * sizeof(float)));
         HIP_TRY(c->W1.ensure((size_t)c->k * c->l_pad * sizeof(float)));
-        HIP_TRY(launch_vt_g(c->V.as<float>(), c->k_ld, c->G.as<float>(), c->l_pad, c->s, c->k,
-                            c->l_pad, c->vt_part.as<float>(), vs, st));
-        HIP_TRY(launch_reduce_scale(c->vt_part.as<float>(), vs, c->k, c->l_pad, c->Dk.as<float>(),
+        const float one = 1.f, zero = 0.f;
+        float* G = c->G.as<float>();
+        const float* V = c->V.as<float>();
+        float* P = c->vt_part.as<float>();
+        rocblas_status gs = rocblas_status_success;
+        if (sfull > 0)
+            gs = rocblas_sgemm_strided_batched(
+                c->blas, rocblas_operation_none, rocblas_operation_transpose,
+                (rocblas_int)c->l_pad, (rocblas_int)c->k, (rocblas_int)kVChunk, &one, G,
+                (rocblas_int)c->l_pad, (rocblas_stride)(kVChunk * c->l_pad), V,
+                (rocblas_int)c->k_ld, (rocblas_stride)(kVChunk * c->k_ld), &zero, P,
+                (rocblas_int)c->l_pad, (rocblas_stride)vslice, (rocblas_int)sfull);
+        if (gs == rocblas_status_success && stail > 0)
+            gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_transpose,
+                               (rocblas_int)c->l_pad, (rocblas_int)c->k, (rocblas_int)stail, &one,
+                               G + sfull * kVChunk * c->l_pad, (rocblas_int)c->l_pad,
+                               V + sfull * kVChunk * c->k_ld, (rocblas_int)c->k_ld, &zero,
+                               P + sfull * vslice, (rocblas_int)c->l_pad);
+        if (gs != rocblas_status_success)
+            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        HIP_TRY(launch_reduce_scale(P, (int)nvs, c->k, c->l_pad, c->Dk.as<float>(),
                                     c->W1.as<float>(), st));
-        HIP_TRY(launch_lowrank_update(c->V.as<float>(), c->k_ld, c->W1.as<float>(), c->l_pad, c->s,
-                                      c->k, c->l, c->r_dev.as<int64_t>(), alpha, c->l_pad,
-                                      (float)coef, st));
+        gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_none,
+                           (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)c->k, &one,
+                           c->W1.as<float>(), (rocblas_int)c->l_pad, V, (rocblas_int)c->k_ld,
+                           &zero, G, (rocblas_int)c->l_pad);
+        if (gs != rocblas_status_success)
+            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
+        HIP_TRY(launch_scatter_add_rows(G, c->l_pad, c->s, c->l, c->r_dev.as<int64_t>(), alpha,
+                                        c->l_pad, (float)coef, st));
     }
     if (c->timing) {
         rc = record(st, c->step_ev, false);

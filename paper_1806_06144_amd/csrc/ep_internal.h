@@ -115,14 +115,14 @@ hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pa
 hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad,
                               int64_t ldw, int64_t rows, int64_t cols, float* out,
                               int64_t ldo, hipStream_t s);
-hipError_t launch_vt_g(const float* V, int64_t ldv, const float* G, int64_t ldg,
-                       int64_t s_rows, int64_t k, int64_t cols_pad, float* part,
-                       int slices, hipStream_t st);
+// W1 = diag(Dk) (sum of the slices of part), slices of round_up(k, 64) x
+// cols_pad row-major, W1 k x cols_pad.
 hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
                                const float* Dk, float* W1, hipStream_t st);
-hipError_t launch_lowrank_update(const float* V, int64_t ldv, const float* W1, int64_t ldw1,
-                                 int64_t s_rows, int64_t k, int64_t l, const int64_t* r,
-                                 float* alpha, int64_t lda, float coef, hipStream_t st);
+// alpha[r[i], j] += coef * H[i, j] for i < rows, j < l; the rows r distinct.
+hipError_t launch_scatter_add_rows(const float* H, int64_t ldh, int64_t rows, int64_t l,
+                                   const int64_t* r, float* alpha, int64_t lda, float coef,
+                                   hipStream_t st);
 hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d,
                                        int kind, double bandwidth, double* Ks,
                                        hipStream_t st);

@@ -11,8 +11,8 @@ namespace ep {
 
 namespace {
 
-constexpr int kGT = 64;     // SIMT GEMM tile edge
-constexpr int kGK = 16;     // SIMT GEMM depth per stage
+constexpr int kGT = 64;     // tile edge of the float64 K_s kernel (and slice padding of k)
+constexpr int kGK = 16;     // its depth per stage
 
 __global__ void __launch_bounds__(256) row_norms_kernel(const float* X, int64_t rows,
                                                         int64_t d, int64_t ld, float* out) {
@@ -89,79 +89,6 @@ __global__ void __launch_bounds__(256) reduce_rows_kernel(const float* part, int
     out[b * ldo + c] = f;
 }
 
-// C(i, j) = sum_kk A(i, kk) B(kk, j) over kk in this block's depth range,
-// A(i, kk) = TA ? A[kk * lda + i] : A[i * lda + kk], B row-major.
-//   EPI 0: store into slice blockIdx.z of C (rows padded to a multiple of 64)
-//   EPI 1: alpha[r[i], j] += coef * C(i, j) for j < nvalid
-struct GemmArgs {
-    int64_t M, N, K, kper;
-    const float* A;
-    int64_t lda;
-    const float* B;
-    int64_t ldb;
-    float* C;
-    int64_t ldc, c_slice;
-    const int64_t* r;
-    float* alpha;
-    int64_t ld_alpha, nvalid;
-    float coef;
-};
-
-template <bool TA, int EPI>
-__global__ void __launch_bounds__(256) gemm_simt_kernel(GemmArgs g) {
-    __shared__ float As[kGK][kGT + 4];
-    __shared__ float Bs[kGK][kGT + 4];
-    const int tid = threadIdx.x;
-    const int tx = tid & 15, ty = tid >> 4;
-    const int64_t i0 = (int64_t)blockIdx.y * kGT;
-    const int64_t j0 = (int64_t)blockIdx.x * kGT;
-    const int64_t kb = (int64_t)blockIdx.z * g.kper;
-    const int64_t ke = min(g.K, kb + g.kper);
-    float acc[4][4] = {};
-    for (int64_t k0 = kb; k0 < ke; k0 += kGK) {
-        for (int e = tid; e < kGK * kGT; e += 256) {
-            const int kk = e / kGT, ii = e % kGT;
-            const int64_t gi = i0 + ii, gk = k0 + kk;
-            float v = 0.f;
-            if (gi < g.M && gk < ke) v = TA ? g.A[gk * g.lda + gi] : g.A[gi * g.lda + gk];
-            As[kk][ii] = v;
-            const int64_t gj = j0 + ii;
-            float w = 0.f;
-            if (gj < g.N && gk < ke) w = g.B[gk * g.ldb + gj];
-            Bs[kk][ii] = w;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < kGK; ++kk) {
-            float a[4], b[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                a[q] = As[kk][ty * 4 + q];
-                b[q] = Bs[kk][tx * 4 + q];
-            }
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) acc[p][q] = fmaf(a[p], b[q], acc[p][q]);
-        }
-        __syncthreads();
-    }
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const int64_t gi = i0 + ty * 4 + p;
-        if (gi >= g.M) continue;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t gj = j0 + tx * 4 + q;
-            if (EPI == 0) {
-                if (gj < g.N) g.C[blockIdx.z * g.c_slice + gi * g.ldc + gj] = acc[p][q];
-            } else {
-                if (gj < g.nvalid) g.alpha[g.r[gi] * g.ld_alpha + gj] += g.coef * acc[p][q];
-            }
-        }
-    }
-}
-
 __global__ void __launch_bounds__(256) reduce_scale_kernel(const float* part, int slices,
                                                            int64_t k, int64_t k_pad,
                                                            int64_t cols, const float* Dk,
@@ -172,6 +99,20 @@ __global__ void __launch_bounds__(256) reduce_scale_kernel(const float* part, in
     float f = 0.f;
     for (int sl = 0; sl < slices; ++sl) f += part[(int64_t)sl * k_pad * cols + e];
     W1[e] = Dk[i] * f;
+}
+
+// alpha[r[i], j] += coef * H[i, j] for i < rows, j < l (the fixed-block
+// update of Algorithm 1 step 5; the rows r are distinct, so no two threads
+// touch one element).
+__global__ void __launch_bounds__(256) scatter_add_rows_kernel(const float* H, int64_t ldh,
+                                                               int64_t rows, int64_t l,
+                                                               const int64_t* r, float* alpha,
+                                                               int64_t lda, float coef) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= rows * l) return;
+    const int64_t i = e / l;
+    const int64_t j = e - i * l;
+    alpha[r[i] * lda + j] += coef * H[i * ldh + j];
 }
 
 // K_s[i, j] = k(x_ri, x_rj) in float64 from direct coordinate differences.
@@ -292,25 +233,6 @@ hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad, i
     return hipGetLastError();
 }
 
-hipError_t launch_vt_g(const float* V, int64_t ldv, const float* G, int64_t ldg, int64_t s_rows,
-                       int64_t k, int64_t cols_pad, float* part, int slices, hipStream_t st) {
-    GemmArgs g{};
-    g.M = k;
-    g.N = cols_pad;
-    g.K = s_rows;
-    g.kper = round_up(ceil_div(s_rows, slices), kGK);
-    g.A = V;
-    g.lda = ldv;
-    g.B = G;
-    g.ldb = ldg;
-    g.C = part;
-    g.ldc = cols_pad;
-    g.c_slice = round_up(k, kGT) * cols_pad;
-    dim3 grid((unsigned)ceil_div(cols_pad, kGT), (unsigned)ceil_div(k, kGT), (unsigned)slices);
-    hipLaunchKernelGGL((gemm_simt_kernel<true, 0>), grid, dim3(256), 0, st, g);
-    return hipGetLastError();
-}
-
 hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
                                const float* Dk, float* W1, hipStream_t st) {
     hipLaunchKernelGGL(reduce_scale_kernel, dim3(blocks_for(k * cols_pad)), dim3(256), 0, st,
@@ -318,25 +240,12 @@ hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t
     return hipGetLastError();
 }
 
-hipError_t launch_lowrank_update(const float* V, int64_t ldv, const float* W1, int64_t ldw1,
-                                 int64_t s_rows, int64_t k, int64_t l, const int64_t* r,
-                                 float* alpha, int64_t lda, float coef, hipStream_t st) {
-    GemmArgs g{};
-    g.M = s_rows;
-    g.N = l;
-    g.K = k;
-    g.kper = round_up(k, kGK);
-    g.A = V;
-    g.lda = ldv;
-    g.B = W1;
-    g.ldb = ldw1;
-    g.r = r;
-    g.alpha = alpha;
-    g.ld_alpha = lda;
-    g.nvalid = l;
-    g.coef = coef;
-    dim3 grid((unsigned)ceil_div(l, kGT), (unsigned)ceil_div(s_rows, kGT), 1);
-    hipLaunchKernelGGL((gemm_simt_kernel<false, 1>), grid, dim3(256), 0, st, g);
+hipError_t launch_scatter_add_rows(const float* H, int64_t ldh, int64_t rows, int64_t l,
+                                   const int64_t* r, float* alpha, int64_t lda, float coef,
+                                   hipStream_t st) {
+    if (rows <= 0 || l <= 0) return hipSuccess;
+    hipLaunchKernelGGL(scatter_add_rows_kernel, dim3(blocks_for(rows * l)), dim3(256), 0, st, H,
+                       ldh, rows, l, r, alpha, lda, coef);
     return hipGetLastError();
 }
 
