@@ -702,10 +702,6 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
 #pragma unroll
                     for (int j = 0; j < 2; ++j) bring[0][j] = rdq(buf, (c + 1) & (kRB - 1), j);
                     mfma_half(cring[c % kRP], 1);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
                 }
                 // refill this ring entry with the chunk kRP positions on
                 if (c + kRP < kRB)
