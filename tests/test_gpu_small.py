@@ -22,7 +22,9 @@ CASES = [
     # wave, one of them partly empty)
     ("laplacian", 3000, 48, 70, 300, 30, 200, 2.0),
     ("gaussian", 2600, 96, 200, 256, 25, 300, 1.5),
-    # a batch of exactly two 512-row chunks for the product of steps 4-5
+    # batches of exactly one and two 512-row chunks for the product of
+    # steps 4-5 (subsample of 192 = 3 x 64 rows for V^T G)
+    ("laplacian", 1200, 32, 5, 192, 20, 512, 1.0),
     ("gaussian", 1500, 32, 5, 200, 20, 1024, 1.0),
 ]
 
