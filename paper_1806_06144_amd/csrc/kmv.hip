@@ -30,6 +30,10 @@
 //      runs on the same MFMA with W read straight from global memory (a few
 //      k-steps ahead). The label tiles are spread over the 8 waves so that
 //      the accumulators of up to 1024 labels fit in 128 registers per lane.
+//   4. Optionally (kpos, step 2 of the vector body) the kernel values of the
+//      centres that are subsample points are also stored, column by column,
+//      so that steps 4-5 need no second pass over those m x s entries (the
+//      paper reads them from its stored block).
 // Partial sums of each split (and centre group, see wl/wj) are written to
 // their own slice and summed by a separate deterministic reduction.
 #include "ep_device.h"
