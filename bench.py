@@ -232,7 +232,7 @@ def study_convergence(args):
                 err = mse()
             rec = {"study": "convergence", "n": cfg.n, "k": k, "m": m, "epochs": epochs,
                    "step_time_s": gpu_s, "train_mse": err, "threshold": thr,
-                   "converged": err < thr}
+                   "converged": err < thr, "m_G": m_G}
             out.append(rec)
             log(json.dumps(rec))
     ep.ep_destroy(ctx)
