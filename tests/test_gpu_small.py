@@ -169,6 +169,24 @@ def test_error_paths_and_alpha_roundtrip():
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("kernel", ["gaussian", "laplacian"])
+def test_predict_over_several_row_chunks(kernel):
+    # 70000 query rows: two full 32768-row prediction chunks and a ragged one
+    n, d, l = 400, 16, 3
+    X, _, a, rng = _problem(n, d, l, 9)
+    a = a * np.sqrt(n)                    # O(1) weights: no cancellation to hide errors in
+    Z = (rng.standard_normal((70000, d)) / np.sqrt(d)).astype(np.float32)
+    r = rng.choice(n, 50, replace=False)
+    with Gpu(X, l, kernel, 1.1, 50, 5, r) as g:
+        g.set_alpha(a)
+        P = g.predict(Z)
+    P_o = oracle.predict(X, a.astype(np.float64), Z, kernel_id(kernel), 1.1)
+    assert rel(P, P_o) < TOL_STEP
+    for z0 in (0, 32767, 32768, 65535, 65536, 69999):   # rows at the chunk seams
+        assert np.allclose(P[z0], P_o[z0], rtol=1e-4, atol=1e-4 * np.abs(P_o).max())
+
+
+@pytest.mark.gpu
 def test_restore_from_saved_setup():
     import paper_1806_06144_amd as ep
     n, d, l, s, k = 900, 20, 6, 150, 15
