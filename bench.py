@@ -106,11 +106,17 @@ def cpu_baseline(X, alpha_host, cfg, target_s=20.0):
             break
         rows = grown
         dt = timed(rows)
+    rate = rows * X.shape[0] / dt
+    n = X.shape[0]
     return {
-        "value": rows * X.shape[0] / dt,
+        "value": rate,
         "unit": "entries/s",
         "cores": int(cores),
         "kind": "oracle",
+        # an epoch evaluates n (n + s) kernel entries (every row against all
+        # centres in step 2 and against the subsample in steps 4-5): the
+        # oracle's epoch at the measured rate, extrapolated, not run
+        "s_per_epoch_extrapolated": n * (n + cfg.s) / rate,
         "sample": (f"fp64 oracle F = K(X_t, X) alpha for {rows} batch rows against all "
                    f"{X.shape[0]} centres (d={X.shape[1]}, l={alpha_host.shape[1]}), "
                    f"{dt:.1f} s"),
