@@ -53,6 +53,12 @@ Readings of the paper (shared with the HIP path by construction)
 * Squared distances use |a|^2 + |b|^2 - 2 a.b in float64 (a matrix product
   as a library step), clamped at zero so that the square root of the
   Laplacian kernel is defined when rounding makes the expansion negative.
+  Where both sides index the same training row (the batch against all
+  centres, the subsample against itself or against the batch) the distance
+  is the direct sum of squared coordinate differences, which is exactly 0:
+  a point's distance to itself is 0 by definition, and the expansion would
+  leave rounding noise there (for the Laplacian kernel k(x, x) ~ 1 - 1e-8,
+  the square root of that noise).
 * Sums over the n centres are accumulated block by block over rows of X.
 
 Parity pins live in tests/test_oracle_*.py.
@@ -73,20 +79,32 @@ def _f64(a):
     return np.asarray(a, dtype=np.float64)
 
 
-def sq_dist(A, B):
-    """All pairwise |a - b|^2 (float64), rows of A against rows of B."""
+def sq_dist(A, B, ids_a=None, ids_b=None):
+    """All pairwise |a - b|^2 (float64), rows of A against rows of B.
+
+    ``ids_a`` / ``ids_b`` (optional, distinct on each side) name the training
+    row behind each row of A and B; pairs with equal ids get the direct sum
+    of squared differences instead of the expansion."""
     A = _f64(A)
     B = _f64(B)
     an = np.einsum("ij,ij->i", A, A)
     bn = np.einsum("ij,ij->i", B, B)
     d2 = an[:, None] + bn[None, :] - 2.0 * (A @ B.T)
     np.maximum(d2, 0.0, out=d2)
+    if ids_a is not None and ids_b is not None:
+        _, pa, pb = np.intersect1d(np.asarray(ids_a, dtype=np.int64),
+                                   np.asarray(ids_b, dtype=np.int64),
+                                   assume_unique=True, return_indices=True)
+        if pa.size:
+            diff = A[pa] - B[pb]
+            d2[pa, pb] = np.einsum("ij,ij->i", diff, diff)
     return d2
 
 
-def kernel_matrix(A, B, kernel, bandwidth):
-    """[k(a_i, b_j)] in float64 (Appendix B kernels)."""
-    d2 = sq_dist(A, B)
+def kernel_matrix(A, B, kernel, bandwidth, ids_a=None, ids_b=None):
+    """[k(a_i, b_j)] in float64 (Appendix B kernels); see ``sq_dist`` for the
+    optional row ids."""
+    d2 = sq_dist(A, B, ids_a, ids_b)
     if kernel == GAUSSIAN:
         return np.exp(-d2 / (2.0 * float(bandwidth) ** 2))
     if kernel == LAPLACIAN:
@@ -94,14 +112,16 @@ def kernel_matrix(A, B, kernel, bandwidth):
     raise ValueError(f"unknown kernel {kernel!r}")
 
 
-def _kernel_times(Q, X, W, kernel, bandwidth, block=_BLOCK):
+def _kernel_times(Q, X, W, kernel, bandwidth, block=_BLOCK, q_ids=None):
     """sum_i k(q, x_i) W_i for every row q of Q, over all rows x_i of X,
-    accumulated block by block over the rows of X."""
+    accumulated block by block over the rows of X. ``q_ids``: the training
+    row of each query, if the queries are training points."""
     Q = _f64(Q)
     out = np.zeros((Q.shape[0], W.shape[1]), dtype=np.float64)
     for a in range(0, X.shape[0], block):
         b = min(X.shape[0], a + block)
-        out += kernel_matrix(Q, X[a:b], kernel, bandwidth) @ _f64(W[a:b])
+        ids = None if q_ids is None else np.arange(a, b)
+        out += kernel_matrix(Q, X[a:b], kernel, bandwidth, q_ids, ids) @ _f64(W[a:b])
     return out
 
 
@@ -152,7 +172,7 @@ def setup(X, kernel, bandwidth, s, k, sub_idx):
     if r.shape != (s,) or not (0 <= k < s <= n):
         raise ValueError("need 0 <= k < s <= n and s subsample indices")
     Xs = _f64(X[r])
-    Ks = kernel_matrix(Xs, Xs, kernel, bandwidth)
+    Ks = kernel_matrix(Xs, Xs, kernel, bandwidth, r, r)
     # top k+1 eigenpairs of K_s (ascending from LAPACK, reversed)
     w, U = scipy.linalg.eigh(Ks, subset_by_index=[s - k - 1, s - 1])
     sigma = w[::-1].copy()
@@ -182,11 +202,11 @@ def step(state, alpha, t, y_b, block=_BLOCK):
     y_b = _f64(y_b)
     Xb = _f64(state.X[t])
     # step 2: f(x_tj) = sum_i alpha_i k(x_i, x_tj)
-    F = _kernel_times(Xb, state.X, alpha, state.kernel, state.bandwidth, block)
+    F = _kernel_times(Xb, state.X, alpha, state.kernel, state.bandwidth, block, q_ids=t)
     R = F - y_b
     c = step_coefficient(state.beta, state.lam, t.shape[0])
     # steps 4-5: sum_i (f(x_ti) - y_ti) V D V^T phi(x_ti)
-    G = kernel_matrix(state.Xs, Xb, state.kernel, state.bandwidth) @ R
+    G = kernel_matrix(state.Xs, Xb, state.kernel, state.bandwidth, state.r, t) @ R
     H = state.V @ (state.D[:, None] * (state.V.T @ G))
     out = alpha.copy()
     out[t] -= c * R                 # step 3
@@ -230,9 +250,10 @@ def step_pointwise(state, alpha, t, y_b):
     return out, f
 
 
-def predict(X, alpha, Z, kernel, bandwidth, block=_BLOCK):
-    """f(z) = sum_i alpha_i k(x_i, z) for every row z of Z."""
-    return _kernel_times(Z, X, _f64(alpha), kernel, bandwidth, block)
+def predict(X, alpha, Z, kernel, bandwidth, block=_BLOCK, z_ids=None):
+    """f(z) = sum_i alpha_i k(x_i, z) for every row z of Z (``z_ids``: the
+    training row of each z, when the points predicted are training points)."""
+    return _kernel_times(Z, X, _f64(alpha), kernel, bandwidth, block, q_ids=z_ids)
 
 
 def run_epoch(state, alpha, batches, y_of):
@@ -245,7 +266,8 @@ def run_epoch(state, alpha, batches, y_of):
 
 def interpolant(X, Y, kernel, bandwidth):
     """alpha* = K^{-1} Y (Section 2), by a dense solve."""
-    K = kernel_matrix(X, X, kernel, bandwidth)
+    ids = np.arange(X.shape[0])
+    K = kernel_matrix(X, X, kernel, bandwidth, ids, ids)
     return np.linalg.solve(K, _f64(Y))
 
 

@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
+from direct_kernel import kmat
 
 
 def _brute(A, B, kernel, bw):
@@ -48,11 +49,31 @@ def test_matches_brute_force(kernel):
 def test_symmetric_unit_diagonal_psd(kernel):
     rng = np.random.default_rng(2)
     X = rng.random((120, 16))
-    K = oracle.kernel_matrix(X, X, kernel, 0.8)
+    ids = np.arange(120)
+    K = oracle.kernel_matrix(X, X, kernel, 0.8, ids, ids)
     np.testing.assert_allclose(K, K.T, rtol=0, atol=1e-15)
-    np.testing.assert_allclose(np.diag(K), 1.0, rtol=0, atol=1e-7)
+    # the same training row on both sides: distance exactly 0, k(x, x) = 1
+    assert np.all(np.diag(K) == 1.0)
     w = np.linalg.eigvalsh(K)
     assert w.min() > -1e-12 * K.shape[0]
+
+
+@pytest.mark.parametrize("kernel", [oracle.GAUSSIAN, oracle.LAPLACIAN])
+def test_matches_direct_differences_with_row_ids(kernel):
+    """Against scipy's cdist (direct differences): a batch of training rows
+    against a block of centres that shares some of them, as in step 2 and
+    steps 4-5. Without ids the Laplacian diagonal carries the square root of
+    the expansion's rounding (~1e-8); with them it is exact."""
+    rng = np.random.default_rng(12)
+    X = rng.random((300, 40)) * 3.0
+    t = rng.choice(300, 50, replace=False)
+    blk = np.arange(100, 260)
+    K = oracle.kernel_matrix(X[t], X[blk], kernel, 2.0, t, blk)
+    ref = kmat(X[t], X[blk], kernel, 2.0)
+    np.testing.assert_allclose(K, ref, rtol=1e-12, atol=0)
+    hit = np.isin(t, blk)
+    assert hit.sum() > 5
+    assert np.all(K[np.nonzero(hit)[0], t[hit] - 100] == 1.0)
 
 
 def test_sq_dist_clamped_and_translation_invariant():

@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
+from direct_kernel import kmat
 from oracle import eigenpro as ep
 
 
@@ -14,13 +15,13 @@ def _mutant(kind):
         t = np.asarray(t, dtype=np.int64)
         alpha = np.asarray(alpha, dtype=np.float64)
         Xb = np.asarray(state.X[t], dtype=np.float64)
-        F = ep._kernel_times(Xb, state.X, alpha, state.kernel, state.bandwidth, block)
+        F = ep._kernel_times(Xb, state.X, alpha, state.kernel, state.bandwidth, block, q_ids=t)
         R = F - y_b
         m = t.shape[0]
         c = ep.step_coefficient(state.beta, state.lam, m)
         if kind == "no_batch_term":
             c = 1.0 / state.beta
-        Ksb = ep.kernel_matrix(state.Xs, Xb, state.kernel, state.bandwidth)
+        Ksb = ep.kernel_matrix(state.Xs, Xb, state.kernel, state.bandwidth, state.r, t)
         if kind == "wrong_row_of_R":
             R_g = R[::-1]
         else:
@@ -54,7 +55,7 @@ def _full_batch_pin(step_fn, k=6):
     st = oracle.setup(X, oracle.GAUSSIAN, 0.8, n, k, r)
     t = rng.permutation(n)
     a1, _ = step_fn(st, a0, t, Y[t])
-    K = oracle.kernel_matrix(X, X, oracle.GAUSSIAN, 0.8)
+    K = kmat(X, X, oracle.GAUSSIAN, 0.8)
     sig, U = np.linalg.eigh(K)
     a_star = np.linalg.solve(K, Y)
     c = 1.0 / (st.beta + (n - 1) * st.sigma[k] / n)

@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
+from direct_kernel import kmat
 
 
 def _data(n=300, d=12, seed=0):
@@ -20,7 +21,7 @@ def test_eigensystem(kernel):
     rng = np.random.default_rng(5)
     r = rng.choice(X.shape[0], 120, replace=False)
     st = oracle.setup(X, kernel, 1.0, 120, 15, r)
-    Ks = oracle.kernel_matrix(X[r], X[r], kernel, 1.0)
+    Ks = kmat(X[r], X[r], kernel, 1.0)
     # eigen-equation residual and orthonormality
     res = Ks @ st.V - st.V * st.sigma[:15]
     assert np.linalg.norm(res) <= 1e-10 * np.linalg.norm(Ks)
@@ -38,8 +39,8 @@ def _kp_diag_brute(st):
     out = []
     for i in range(st.s):
         x = st.Xs[i:i + 1]
-        phi = oracle.kernel_matrix(st.Xs, x, st.kernel, st.bandwidth)[:, 0]
-        kxx = oracle.kernel_matrix(x, x, st.kernel, st.bandwidth)[0, 0]
+        phi = kmat(st.Xs, x, st.kernel, st.bandwidth)[:, 0]
+        kxx = kmat(x, x, st.kernel, st.bandwidth)[0, 0]
         out.append(kxx - phi @ P @ phi)
     return np.array(out)
 
@@ -67,7 +68,7 @@ def test_nystrom_identities_full_subsample():
     # unit RKHS norm: (1/sigma_i) v_i^T K v_i = 1
     X = _data(80, 5, 3)
     st = oracle.setup(X, oracle.GAUSSIAN, 1.0, 80, 10, np.arange(80))
-    K = oracle.kernel_matrix(X, X, oracle.GAUSSIAN, 1.0)
+    K = kmat(X, X, oracle.GAUSSIAN, 1.0)
     for i in range(10):
         v = st.V[:, i]
         assert (v @ K @ v) / st.sigma[i] == pytest.approx(1.0, rel=1e-12)
@@ -88,7 +89,7 @@ def test_q_equals_k_plus_one_form():
     # the paper's D with q = k+1 columns has D_qq = 0, so V D V^T is the same
     X = _data(120, 6, 5)
     st = oracle.setup(X, oracle.GAUSSIAN, 1.0, 60, 9, np.arange(60))
-    Ks = oracle.kernel_matrix(X[:60], X[:60], oracle.GAUSSIAN, 1.0)
+    Ks = kmat(X[:60], X[:60], oracle.GAUSSIAN, 1.0)
     w, U = np.linalg.eigh(Ks)
     w, U = w[::-1][:10], U[:, ::-1][:, :10]
     Dq = (1.0 - w[9] / w) / w          # Sigma^-1 (1 - sigma_q Sigma^-1), q = 10

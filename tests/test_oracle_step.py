@@ -20,6 +20,7 @@ import numpy as np
 import pytest
 
 import oracle
+from direct_kernel import kmat
 
 
 def _problem(n=60, d=6, l=3, seed=0):
@@ -36,7 +37,7 @@ def test_k0_is_plain_sgd(kernel):
     st = oracle.setup(X, kernel, 0.9, 30, 0, np.arange(0, 60, 2))
     t = np.array([3, 17, 40, 41, 59, 8])
     a1, F = oracle.step(st, a0, t, Y[t])
-    K = oracle.kernel_matrix(X, X, kernel, 0.9)
+    K = kmat(X, X, kernel, 0.9)
     c = 1.0 / (1.0 + (len(t) - 1) * st.sigma[0] / 30)
     expect = a0.copy()
     expect[t] -= c * ((K @ a0)[t] - Y[t])
@@ -63,7 +64,7 @@ def test_full_batch_flattened_spectrum(kernel, k):
     st = oracle.setup(X, kernel, 0.8, n, k, r)
     t = rng.permutation(n)                  # full batch, another order
     a1, _ = oracle.step(st, a0, t, Y[t])
-    K = oracle.kernel_matrix(X, X, kernel, 0.8)
+    K = kmat(X, X, kernel, 0.8)
     sig, U = np.linalg.eigh(K)
     a_star = np.linalg.solve(K, Y)
     c = oracle.step_coefficient(st.beta, st.lam, n)
