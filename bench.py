@@ -363,8 +363,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--contraction", choices=["auto", "fused", "blocked"], default="auto",
                     help="form of F = K(X_t, X) alpha timed for the headline (ep_set_contraction)")
-    ap.add_argument("--no-blocked-compare", action="store_true",
-                    help="skip timing the blocked form next to the default fused one")
+    ap.add_argument("--blocked-compare", action="store_true",
+                    help="also time the opt-in blocked form (kernel block written per centre "
+                         "chunk) on the same batches, after the headline")
     ap.add_argument("--s", type=int, default=None,
                     help="override the subsample size (experiments only)")
     ap.add_argument("--shard", type=int, default=1,
@@ -509,7 +510,7 @@ def main():
     # the blocked form on the same batches, for comparison (not the headline:
     # it writes the kernel block to memory)
     blocked_form = None
-    if args.contraction != "blocked" and not args.no_blocked_compare and cfg.d % 4 == 0:
+    if args.contraction != "blocked" and args.blocked_compare and cfg.d % 4 == 0:
         ep.ep_set_contraction(ctx, "blocked")
         ep.ep_step(ctx, t_dev[0], m, y_dev[0])
         ep.ep_sync(ctx)

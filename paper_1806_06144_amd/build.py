@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libeigenpro.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["api.hip", "kmv.hip", "kblock.hip", "kernels.hip", "probe.hip", "eigsolve.hip"]
+SOURCES = ["api.hip", "kmv.hip", "kblock.hip", "kernels.hip", "thin_gemm.hip", "probe.hip",
+           "eigsolve.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

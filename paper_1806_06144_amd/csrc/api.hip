@@ -60,7 +60,8 @@ struct ep_ctx {
     int64_t l_pad = 0, n_pad = 0, s_pad = 0, k_ld = 1;
     ep_info info{};
     std::vector<double> sigma, D;       // sigma: k_max+1 values; D: k values
-    std::vector<float> Vh;              // host copy of V (s x k_max)
+    std::vector<float> Vh;              // host copy of V (s x k_max, float32 as applied)
+    std::vector<double> Vh64;           // float64 eigenvectors (s x k_max): beta, Eq. 7 sums
     std::vector<int64_t> r_host;
     ep_setup_opts opts{};               // eigensolver choice of ep_setup_ex
     uint64_t seed = 0;
@@ -106,11 +107,6 @@ constexpr size_t kPartBudget = size_t(2) << 30;   // bytes of split partial sums
 // the separate subsample pass (and the capture must stay below 2^31 bytes,
 // the reach of its buffer descriptor)
 constexpr size_t kKsbBudget = (size_t(2) << 30) - 256;
-constexpr int64_t kGChunk = 512;   // batch rows per GEMM of steps 4-5
-// subsample rows per partial product V^T G: the top eigenvector's component
-// of G sums terms that largely cancel, and predictions scale its rounding
-// error by the kernel's largest eigenvalue, so its sums are kept short
-constexpr int64_t kVChunk = 64;
 
 int max_slices_for(int64_t rows_pad, int64_t ldw) {
     const size_t per = (size_t)rows_pad * (size_t)ldw * sizeof(float);
@@ -279,10 +275,8 @@ int run_main_pass(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const
 // subsample columns for steps 4-5: fused form, vector body, and the capture
 // buffer and the product's partial slices within budget.
 bool capture_subsample(const ep_ctx* c, const float* xb, int64_t m) {
-    const size_t g_slices = (size_t)ceil_div(m, kGChunk) * c->s * c->l_pad * sizeof(float);
     return c->k > 0 && !use_blocked(c, xb, c->d) && kmv_vec(xb, c->d, c->X, c->d, c->d) &&
-           (size_t)c->s * (size_t)round_up(m, kBM) * sizeof(float) <= kKsbBudget &&
-           g_slices <= kPartBudget;
+           (size_t)c->s * (size_t)round_up(m, kBM) * sizeof(float) <= kKsbBudget;
 }
 
 struct DeviceGuard {
@@ -302,7 +296,7 @@ struct DeviceGuard {
 // Chebyshev-filtered subspace iteration of eigsolve.hip (Section 4 needs
 // only the top k+1 pairs). Fills c->sigma, c->V and the adapted kernel's
 // diagonal k_G(x_ri, x_ri) at the subsample points.
-int eigensystem_from_solver(ep_ctx* c, std::vector<double>& kpd) {
+int eigensystem_from_solver(ep_ctx* c) {
     const int64_t s = c->s, k = c->k, d = c->d;
     hipStream_t st = c->stream;
     const ep_setup_opts& o = c->opts;
@@ -318,10 +312,8 @@ int eigensystem_from_solver(ep_ctx* c, std::vector<double>& kpd) {
         // measured crossover: the dense solve's O(s^3) wins below s ~ 16 p
         solver = (s >= 2048 && 16 * (q + guard) <= s) ? EP_SOLVER_SUBSPACE : EP_SOLVER_DENSE;
     }
-    DevBuf Ks, W, E, kp, sig_dev, iinfo, Vq;
+    DevBuf Ks, W, E, iinfo, Vq;
     HIP_TRY(Ks.ensure((size_t)s * s * sizeof(double)));
-    HIP_TRY(kp.ensure((size_t)s * sizeof(double)));
-    HIP_TRY(sig_dev.ensure((size_t)(k + 1) * sizeof(double)));
     HIP_TRY(launch_subsample_kernel_f64(c->Xs.as<float>(), s, d, c->kind, c->bandwidth,
                                         Ks.as<double>(), st));
 
@@ -388,20 +380,28 @@ int eigensystem_from_solver(ep_ctx* c, std::vector<double>& kpd) {
     }
     if (!(c->sigma[k] > 0.0) || !std::isfinite(c->sigma[0]))
         return fail(EP_ENUMERIC, "sigma_{k+1} = %g is not positive", c->sigma[k]);
-    HIP_TRY(hipMemcpyAsync(sig_dev.p, c->sigma.data(), (k + 1) * sizeof(double),
-                           hipMemcpyHostToDevice, st));
-    HIP_TRY(launch_extract_eigvecs(Z, s, col0, col_step, s, k, sig_dev.as<double>(),
-                                   c->V.as<float>(), c->k_ld, kp.as<double>(), st));
-    kpd.resize(s);
-    HIP_TRY(hipMemcpyAsync(kpd.data(), kp.p, s * sizeof(double), hipMemcpyDeviceToHost, st));
+    HIP_TRY(launch_extract_eigvecs(Z, s, col0, col_step, s, k, c->V.as<float>(), c->k_ld, st));
+    // the float64 eigenvectors on the host (row-major s x k), from which
+    // beta and the rank sums of Eq. 7 are formed without float32 rounding
+    c->Vh64.assign((size_t)s * k, 0.0);
+    if (k > 0) {
+        const double* lo = col_step > 0 ? Z + col0 * s : Z + (col0 - (k - 1)) * s;
+        std::vector<double> cols((size_t)s * k);
+        HIP_TRY(hipMemcpyAsync(cols.data(), lo, (size_t)s * k * sizeof(double),
+                               hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipStreamSynchronize(st));
+        for (int64_t j = 0; j < k; ++j) {
+            const int64_t cj = col_step > 0 ? j : (k - 1 - j);
+            for (int64_t i = 0; i < s; ++i) c->Vh64[(size_t)i * k + j] = cols[(size_t)cj * s + i];
+        }
+    }
     HIP_TRY(hipStreamSynchronize(st));
     return EP_OK;
 }
 
 // Eigensystem handed in by the caller (a saved setup): sigma descending,
 // V row-major s x k.
-int eigensystem_from_saved(ep_ctx* c, const double* sigma, const float* V,
-                           std::vector<double>& kpd) {
+int eigensystem_from_saved(ep_ctx* c, const double* sigma, const float* V) {
     const int64_t s = c->s, k = c->k;
     c->sigma.assign(sigma, sigma + k + 1);
     for (int64_t i = 0; i <= k; ++i) {
@@ -410,19 +410,16 @@ int eigensystem_from_saved(ep_ctx* c, const double* sigma, const float* V,
     }
     if (!(c->sigma[k] > 0.0)) return fail(EP_EINVAL, "sigma_{k+1} must be positive");
     if (k > 0 && !V) return fail(EP_EINVAL, "V is NULL");
-    kpd.assign(s, 1.0);
-    for (int64_t i = 0; i < s; ++i) {
-        double acc = 0.0;
-        for (int64_t j = 0; j < k; ++j) {
-            const double v = V[i * k + j];
-            if (!std::isfinite(v)) return fail(EP_EINVAL, "V holds a non-finite value");
-            acc += (c->sigma[j] - c->sigma[k]) * v * v;
-        }
-        kpd[i] = 1.0 - acc;
+    c->Vh64.assign((size_t)s * k, 0.0);
+    for (int64_t i = 0; i < s * k; ++i) {
+        if (!std::isfinite(V[i])) return fail(EP_EINVAL, "V holds a non-finite value");
+        c->Vh64[(size_t)i] = V[i];
     }
-    if (k > 0)
-        HIP_TRY(hipMemcpyAsync(c->V.p, V, (size_t)s * k * sizeof(float), hipMemcpyHostToDevice,
-                               c->stream));
+    if (k > 0) {
+        HIP_TRY(hipMemsetAsync(c->V.p, 0, (size_t)s * c->k_ld * sizeof(float), c->stream));
+        HIP_TRY(hipMemcpy2DAsync(c->V.p, c->k_ld * sizeof(float), V, k * sizeof(float),
+                                 k * sizeof(float), s, hipMemcpyHostToDevice, c->stream));
+    }
     HIP_TRY(hipStreamSynchronize(c->stream));
     return EP_OK;
 }
@@ -442,7 +439,7 @@ std::vector<double> beta_all_ranks(const ep_ctx* c) {
         beta[kk] = kk == 0 ? 1.0 : best;
         if (kk < km) {
             for (int64_t i = 0; i < s; ++i) {
-                const double v = c->Vh[(size_t)i * km + kk];
+                const double v = c->Vh64[(size_t)i * km + kk];
                 A[i] += c->sigma[kk] * v * v;
                 B[i] += v * v;
             }
@@ -472,7 +469,7 @@ int apply_rank(ep_ctx* c, int64_t k) {
         for (int64_t i = 0; i < s; ++i) {
             double acc = 0.0;
             for (int64_t j = 0; j < k; ++j) {
-                const double v = c->Vh[(size_t)i * km + j];
+                const double v = c->Vh64[(size_t)i * km + j];
                 acc += (c->sigma[j] - c->sigma[k]) * v * v;
             }
             beta = std::max(beta, 1.0 - acc);
@@ -502,7 +499,6 @@ int apply_rank(ep_ctx* c, int64_t k) {
 
 int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sigma_in,
              const float* V_in) {
-    std::vector<double> kpd;
     const int64_t n = c->n, d = c->d, s = c->s, k = c->k;
     hipStream_t st = c->stream;
 
@@ -533,19 +529,21 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sig
     c->l_pad = round_up(c->l, kTile);
     c->n_pad = round_up(n, kBN);
     c->s_pad = round_up(s, kBM);
-    c->k_ld = std::max<int64_t>(k, 1);
+    c->k_ld = round_up(std::max<int64_t>(k, 1), 4);   // 16-byte rows for the thin products
 
     HIP_TRY(c->err.ensure(sizeof(int)));
     HIP_TRY(hipMemsetAsync(c->err.p, 0, sizeof(int), st));
     HIP_TRY(c->norms.ensure((size_t)c->n_pad * sizeof(float)));
-    HIP_TRY(c->alpha.ensure((size_t)c->n_pad * c->l_pad * sizeof(float)));
+    // (alpha and R serve as the weights of fused passes: kWeightTail bytes
+    // after the padded rows)
+    HIP_TRY(c->alpha.ensure((size_t)c->n_pad * c->l_pad * sizeof(float) + kWeightTail));
     HIP_TRY(c->r_dev.ensure((size_t)s * sizeof(int64_t)));
     HIP_TRY(c->Xs.ensure((size_t)c->s_pad * d * sizeof(float)));
     HIP_TRY(c->xs_norms.ensure((size_t)c->s_pad * sizeof(float)));
     HIP_TRY(c->V.ensure((size_t)s * c->k_ld * sizeof(float)));
     HIP_TRY(c->Dk.ensure((size_t)c->k_ld * sizeof(float)));
 
-    HIP_TRY(launch_fill_f32(c->alpha.as<float>(), c->n_pad * c->l_pad, 0.f, st));
+    HIP_TRY(launch_fill_f32(c->alpha.as<float>(), c->n_pad * c->l_pad + kWeightTail / 4, 0.f, st));
     HIP_TRY(launch_fill_f32(c->norms.as<float>(), c->n_pad, 0.f, st));
     HIP_TRY(hipMemcpyAsync(c->r_dev.p, c->r_host.data(), s * sizeof(int64_t),
                            hipMemcpyHostToDevice, st));
@@ -563,28 +561,117 @@ int do_setup(ep_ctx* c, const int64_t* sub_idx, uint64_t seed, const double* sig
                                c->s_pad, c->Xs.as<float>(), c->xs_norms.as<float>(),
                                c->err.as<int>(), st));
 
-    int rc = sigma_in ? eigensystem_from_saved(c, sigma_in, V_in, kpd)
-                      : eigensystem_from_solver(c, kpd);
+    int rc = sigma_in ? eigensystem_from_saved(c, sigma_in, V_in) : eigensystem_from_solver(c);
     if (rc) return rc;
 
     int herr = 0;
     HIP_TRY(hipMemcpyAsync(&herr, c->err.p, sizeof(int), hipMemcpyDeviceToHost, st));
     c->Vh.resize((size_t)s * k);
     if (k > 0)
-        HIP_TRY(hipMemcpyAsync(c->Vh.data(), c->V.p, (size_t)s * k * sizeof(float),
-                               hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipMemcpy2DAsync(c->Vh.data(), k * sizeof(float), c->V.p, c->k_ld * sizeof(float),
+                                 k * sizeof(float), s, hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
     if (herr) return fail(EP_EINVAL, "subsample index out of range");
-    (void)kpd;
     c->k_max = k;
     return apply_rank(c, k);
+}
+
+// Steps 4-5 (Algorithm 1, Eq. 8): alpha_r += coef V D V^T K(X_r, X_t) R on
+// the hand-written thin products of thin_gemm.hip. With the subsample
+// columns kept by step 2 (`capture`: c->ksb, s x round_up(m, kBM)) the
+// product is associated in whichever order takes fewer flops:
+//   G first: G = K R (s x l), W = D V^T G       2 s m l + 2 k s l
+//   U first: U = V^T K (k x m), W = D U R       2 k s m + 2 k m l
+// (U first wins when l > k, e.g. 1000 labels at rank 200). Otherwise the
+// subsample pass of the fused kernel forms G = K(X_r, X_t) R directly.
+// Then alpha_r += coef V W, added by the last product's epilogue.
+int subsample_correction(ep_ctx* c, bool capture, const float* xb, const float* xbn,
+                         const int64_t* t, int64_t m, const float* R, float coef) {
+    hipStream_t st = c->stream;
+    const int64_t s = c->s, k = c->k, L = c->l_pad, kld = c->k_ld;
+    const int64_t ldk = round_up(m, kBM);
+    const int groups = 1024;
+    const float* V = c->V.as<float>();
+    // partial slices of one product into c->part, summed (and scaled) into out
+    auto product = [&](const float* A, int64_t lda, bool a_t, const float* B, int64_t ldb,
+                       int64_t M, int64_t N, int64_t K, const float* Dk, float* out,
+                       int64_t ldo) -> int {
+        const ThinGemmPlan pl = thin_gemm_plan(M, N, K, groups);
+        const int64_t slice = M * ldo;
+        const bool direct = pl.chunks == 1 && !Dk;
+        if (!direct) HIP_TRY(c->part.ensure((size_t)pl.chunks * slice * sizeof(float)));
+        ThinGemmArgs g{};
+        g.A = A;
+        g.lda = lda;
+        g.B = B;
+        g.ldb = ldb;
+        g.M = M;
+        g.N = N;
+        g.K = K;
+        g.C = direct ? out : c->part.as<float>();
+        g.ldc = ldo;
+        g.slice = slice;
+        HIP_TRY(thin_gemm_launch(g, pl, a_t, false, st));
+        if (!direct)
+            HIP_TRY(launch_sum_slices(c->part.as<float>(), pl.chunks, slice, M, N, ldo, Dk, out,
+                                      ldo, st));
+        return EP_OK;
+    };
+    int rc = EP_OK;
+    HIP_TRY(c->W1.ensure((size_t)k * L * sizeof(float)));
+    float* W = c->W1.as<float>();
+    const double g_first = (double)s * m * L + (double)k * s * L;
+    const double u_first = (double)k * s * m + (double)k * m * L;
+    if (capture && u_first < g_first) {
+        HIP_TRY(c->G.ensure((size_t)k * ldk * sizeof(float)));
+        float* U = c->G.as<float>();
+        if ((rc = product(V, kld, true, c->ksb.as<float>(), ldk, k, m, s, nullptr, U, ldk)))
+            return rc;
+        if ((rc = product(U, ldk, false, R, L, k, L, m, c->Dk.as<float>(), W, L))) return rc;
+    } else {
+        HIP_TRY(c->G.ensure((size_t)s * L * sizeof(float)));
+        float* G = c->G.as<float>();
+        if (capture) {
+            if ((rc = product(c->ksb.as<float>(), ldk, false, R, L, s, L, m, nullptr, G, L)))
+                return rc;
+        } else {
+            int slices = 0;
+            int64_t rows_pad = 0;
+            rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(),
+                         c->r_dev.as<int64_t>(), s, xb, c->d, xbn, t, m, R, &slices, &rows_pad,
+                         false, true);
+            if (rc) return rc;
+            HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, L, s, L, G, L, st));
+        }
+        if ((rc = product(V, kld, true, G, L, k, L, s, c->Dk.as<float>(), W, L))) return rc;
+    }
+    // alpha_r += coef V W (depth k, one chunk; rows r are distinct)
+    ThinGemmArgs g{};
+    g.A = V;
+    g.lda = kld;
+    g.B = W;
+    g.ldb = L;
+    g.M = s;
+    g.N = L;
+    g.K = k;
+    g.alpha = c->alpha.as<float>();
+    g.ldalpha = L;
+    g.r = c->r_dev.as<int64_t>();
+    g.coef = coef;
+    g.N_valid = c->l;
+    ThinGemmPlan one;
+    one.kc = round_up(k, 64);
+    one.chunks = 1;
+    one.tiles = ceil_div(s, 64) * ceil_div(L, 64);
+    HIP_TRY(thin_gemm_launch(g, one, false, true, st));
+    return EP_OK;
 }
 
 int ensure_step_buffers(ep_ctx* c, int64_t m) {
     const int64_t m_pad = round_up(m, kBN);
     HIP_TRY(c->xb.ensure((size_t)m_pad * c->d * sizeof(float)));
     HIP_TRY(c->xb_norms.ensure((size_t)m_pad * sizeof(float)));
-    HIP_TRY(c->R.ensure((size_t)m_pad * c->l_pad * sizeof(float)));
+    HIP_TRY(c->R.ensure((size_t)m_pad * c->l_pad * sizeof(float) + kWeightTail));
     return EP_OK;
 }
 
@@ -731,96 +818,8 @@ int ep_step(ep_ctx* c, const int64_t* t, int64_t m, const float* y_b, float* f_o
     HIP_TRY(launch_reduce_residual(c->part.as<float>(), slices, rows_pad, c->l_pad, m, c->l, y_b,
                                    f_out, R, m_pad, alpha, c->n, t, (float)coef, st));
     if (c->k > 0) {
-        // steps 4-5: G = K(X_r, X_t) R; alpha_r += c V D V^T G
-        HIP_TRY(c->G.ensure((size_t)c->s * c->l_pad * sizeof(float)));
-        if (capture) {
-            // from the captured columns: G^T = R^T K(X_r, X_t)^T (column-major
-            // view: R^T is l_pad x m, ksb holds K^T as m x s), split over
-            // the batch into chunks of kGChunk rows with one partial slice
-            // each (strided-batched, so the chunks' tiles fill the chip
-            // together), then summed: a library GEMM sums its whole depth in
-            // one float32 chain, so the depth is kept short as the
-            // subsample pass keeps its centre splits short
-            if ((rc = ensure_blas(c))) return rc;
-            const int64_t full = m / kGChunk, tail = m - full * kGChunk;
-            const int64_t nsl = full + (tail > 0 ? 1 : 0);
-            const size_t slice = (size_t)c->s * c->l_pad;
-            float* dst = nsl == 1 ? c->G.as<float>() : nullptr;
-            if (nsl > 1) {
-                HIP_TRY(c->part.ensure((size_t)nsl * slice * sizeof(float)));
-                dst = c->part.as<float>();
-            }
-            const float one = 1.f, zero = 0.f;
-            rocblas_status gs = rocblas_status_success;
-            if (full > 0)
-                gs = rocblas_sgemm_strided_batched(
-                    c->blas, rocblas_operation_none, rocblas_operation_none,
-                    (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)kGChunk, &one, R,
-                    (rocblas_int)c->l_pad, (rocblas_stride)(kGChunk * c->l_pad),
-                    c->ksb.as<float>(), (rocblas_int)rows_pad, (rocblas_stride)kGChunk, &zero,
-                    dst, (rocblas_int)c->l_pad, (rocblas_stride)slice, (rocblas_int)full);
-            if (gs == rocblas_status_success && tail > 0)
-                gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_none,
-                                   (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)tail,
-                                   &one, R + full * kGChunk * c->l_pad, (rocblas_int)c->l_pad,
-                                   c->ksb.as<float>() + full * kGChunk, (rocblas_int)rows_pad,
-                                   &zero, dst + full * slice, (rocblas_int)c->l_pad);
-            if (gs != rocblas_status_success)
-                return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
-            if (nsl > 1)
-                HIP_TRY(launch_reduce_rows(c->part.as<float>(), (int)nsl, c->s, c->l_pad, c->s,
-                                           c->l_pad, c->G.as<float>(), c->l_pad, st));
-        } else {
-            rc = run_kmv(c, c->Xs.as<float>(), c->d, c->xs_norms.as<float>(),
-                         c->r_dev.as<int64_t>(), c->s, xb, c->d, xbn, t, m, R, &slices,
-                         &rows_pad, false, true);
-            if (rc) return rc;
-            HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, c->s,
-                                       c->l_pad, c->G.as<float>(), c->l_pad, st));
-        }
-        // W = D V^T G: partial products over kVChunk-row chunks of the
-        // subsample (strided-batched; column-major view: slice j is
-        // G_j^T V_j, G_j^T l_pad x kVChunk, V_j^T k_ld x kVChunk), summed
-        // and scaled by D; then H = V W on the matrix cores (H^T = W^T V^T,
-        // depth k) into G's buffer, which W no longer needs, and
-        // alpha_r += c H
-        if ((rc = ensure_blas(c))) return rc;
-        const int64_t k_pad = round_up(c->k, 64);
-        const int64_t sfull = c->s / kVChunk, stail = c->s - sfull * kVChunk;
-        const int64_t nvs = sfull + (stail > 0 ? 1 : 0);
-        const size_t vslice = (size_t)k_pad * c->l_pad;
-        HIP_TRY(c->vt_part.ensure((size_t)nvs * vslice * sizeof(float)));
-        HIP_TRY(c->W1.ensure((size_t)c->k * c->l_pad * sizeof(float)));
-        const float one = 1.f, zero = 0.f;
-        float* G = c->G.as<float>();
-        const float* V = c->V.as<float>();
-        float* P = c->vt_part.as<float>();
-        rocblas_status gs = rocblas_status_success;
-        if (sfull > 0)
-            gs = rocblas_sgemm_strided_batched(
-                c->blas, rocblas_operation_none, rocblas_operation_transpose,
-                (rocblas_int)c->l_pad, (rocblas_int)c->k, (rocblas_int)kVChunk, &one, G,
-                (rocblas_int)c->l_pad, (rocblas_stride)(kVChunk * c->l_pad), V,
-                (rocblas_int)c->k_ld, (rocblas_stride)(kVChunk * c->k_ld), &zero, P,
-                (rocblas_int)c->l_pad, (rocblas_stride)vslice, (rocblas_int)sfull);
-        if (gs == rocblas_status_success && stail > 0)
-            gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_transpose,
-                               (rocblas_int)c->l_pad, (rocblas_int)c->k, (rocblas_int)stail, &one,
-                               G + sfull * kVChunk * c->l_pad, (rocblas_int)c->l_pad,
-                               V + sfull * kVChunk * c->k_ld, (rocblas_int)c->k_ld, &zero,
-                               P + sfull * vslice, (rocblas_int)c->l_pad);
-        if (gs != rocblas_status_success)
-            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
-        HIP_TRY(launch_reduce_scale(P, (int)nvs, c->k, c->l_pad, c->Dk.as<float>(),
-                                    c->W1.as<float>(), st));
-        gs = rocblas_sgemm(c->blas, rocblas_operation_none, rocblas_operation_none,
-                           (rocblas_int)c->l_pad, (rocblas_int)c->s, (rocblas_int)c->k, &one,
-                           c->W1.as<float>(), (rocblas_int)c->l_pad, V, (rocblas_int)c->k_ld,
-                           &zero, G, (rocblas_int)c->l_pad);
-        if (gs != rocblas_status_success)
-            return fail(EP_EDEVICE, "rocblas_sgemm returned status %d", (int)gs);
-        HIP_TRY(launch_scatter_add_rows(G, c->l_pad, c->s, c->l, c->r_dev.as<int64_t>(), alpha,
-                                        c->l_pad, (float)coef, st));
+        rc = subsample_correction(c, capture, xb, xbn, t, m, R, (float)coef);
+        if (rc) return rc;
     }
     if (c->timing) {
         rc = record(st, c->step_ev, false);

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace ep {
 
 // Tile geometry of the fused kernel-block contraction (kmv.hip). kBN is
@@ -15,6 +17,11 @@ constexpr int kCSub = 8;                  // centre sub-tiles per iteration
 constexpr int kBM = kTile * kQSub;        // query rows per workgroup (64)
 constexpr int kBN = kTile * kCSub;        // centres per iteration (256)
 constexpr int kThreads = 512;             // 8 waves of 64
+
+// Bytes every weight matrix of a fused pass carries past its last padded
+// row: with three label tiles per wave one 16-byte load fetches three
+// weights and drops the fourth, which can lie up to 12 bytes past the row.
+constexpr int kWeightTail = 16;
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -33,8 +40,9 @@ struct KmvArgs {
     const int64_t* cid;    // global row id of each centre (NULL: j itself)
     int64_t nc;
     int64_t d;
-    const float* W;        // weights, >= round_up(nc, kBN) rows x ldw,
-    int64_t ldw;           //   rows >= nc and columns >= l are zero
+    const float* W;        // weights, >= round_up(nc, kBN) rows x ldw and
+    int64_t ldw;           //   kWeightTail readable bytes after them;
+                           //   rows >= nc and columns >= l are zero
     int lt;                // label tiles = ldw / 32
     float* out;            // partials [slices][out_rows][ldw]
     int64_t out_rows;      // >= round_up(nq, kBM)
@@ -100,6 +108,46 @@ struct KblockArgs {
 };
 hipError_t kblock_launch(const KblockArgs& a, hipStream_t s);
 
+// Thin products of steps 4-5 (thin_gemm.hip):
+//   C[p] = sum over depth chunk p of A(i, kk) B(kk, j), i < M, j < N,
+// B row-major (K x N, ldb); A row-major (M x K, lda) or, with a_t, the
+// transpose of a row-major K x M matrix (A(i, kk) = A[kk lda + i]). Partial
+// slice p goes to C + p slice (row-major, ldc). With `scatter` (one depth
+// chunk only) the result is added instead, times coef, into
+// alpha[r[i] ldalpha + j] for j < N_valid. Leading dimensions must be
+// multiples of 4 floats and A, B 16-byte aligned.
+struct ThinGemmArgs {
+    const float* A;
+    int64_t lda;
+    const float* B;
+    int64_t ldb;
+    int64_t M, N, K;
+    int64_t kc;            // depth per chunk (set from the plan)
+    float* C;
+    int64_t ldc;
+    int64_t slice;         // floats between partial slices
+    float* alpha;          // scatter epilogue
+    int64_t ldalpha;
+    const int64_t* r;
+    float coef;
+    int64_t N_valid;
+};
+struct ThinGemmPlan {
+    int64_t kc = 0;        // depth per chunk, a multiple of the 64-deep accumulation block
+    int chunks = 1;        // partial slices
+    int64_t tiles = 0;
+};
+// Depth chunks so that tiles x chunks reaches min_groups workgroups (each
+// chunk at least 256 deep, at most 64 chunks).
+ThinGemmPlan thin_gemm_plan(int64_t M, int64_t N, int64_t K, int min_groups);
+hipError_t thin_gemm_launch(const ThinGemmArgs& a, const ThinGemmPlan& pl, bool a_t, bool scatter,
+                            hipStream_t st);
+// out[i, j] = Dk[i] * sum_p part[p slice + i ld + j] (no scale when Dk is
+// NULL), for i < rows, j < cols; slices summed in order.
+hipError_t launch_sum_slices(const float* part, int slices, int64_t slice, int64_t rows,
+                             int64_t cols, int64_t ld, const float* Dk, float* out, int64_t ldo,
+                             hipStream_t st);
+
 // Auxiliary kernels (kernels.hip).
 hipError_t launch_row_norms(const float* X, int64_t rows, int64_t d, int64_t ld,
                             float* out, hipStream_t s);
@@ -115,22 +163,13 @@ hipError_t launch_reduce_residual(const float* part, int slices, int64_t rows_pa
 hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad,
                               int64_t ldw, int64_t rows, int64_t cols, float* out,
                               int64_t ldo, hipStream_t s);
-// W1 = diag(Dk) (sum of the slices of part), slices of round_up(k, 64) x
-// cols_pad row-major, W1 k x cols_pad.
-hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
-                               const float* Dk, float* W1, hipStream_t st);
-// alpha[r[i], j] += coef * H[i, j] for i < rows, j < l; the rows r distinct.
-hipError_t launch_scatter_add_rows(const float* H, int64_t ldh, int64_t rows, int64_t l,
-                                   const int64_t* r, float* alpha, int64_t lda, float coef,
-                                   hipStream_t st);
 hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d,
                                        int kind, double bandwidth, double* Ks,
                                        hipStream_t st);
 // V[i, j] = Z[i + (col0 + j col_step) ldz] (float32, row-major, ldv) for
-// j < k, zero for k <= j < ldv; kp_diag[i] = 1 - sum_j (sig_j - sig_k) V_ij^2.
+// j < k, zero for k <= j < ldv.
 hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t col0, int64_t col_step,
-                                  int64_t s, int64_t k, const double* sigma_desc_dev, float* V,
-                                  int64_t ldv, double* kp_diag, hipStream_t st);
+                                  int64_t s, int64_t k, float* V, int64_t ldv, hipStream_t st);
 hipError_t launch_fill_f32(float* p, int64_t count, float v, hipStream_t st);
 
 }  // namespace ep

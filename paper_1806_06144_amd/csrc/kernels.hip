@@ -1,8 +1,7 @@
 // Auxiliary kernels of the EigenPro 2.0 step on gfx950: row norms, batch
 // gather, the deterministic split reduction fused with the residual and the
-// batch-block update (Algorithm 1 step 3), the rank-k correction applied to
-// the fixed block (Algorithm 1 step 5, Eq. 8), and the float64 subsample
-// kernel matrix of the initialisation.
+// batch-block update (Algorithm 1 step 3), and the float64 subsample kernel
+// matrix of the initialisation.
 #include "ep_internal.h"
 
 #include <math.h>
@@ -11,7 +10,7 @@ namespace ep {
 
 namespace {
 
-constexpr int kGT = 64;     // tile edge of the float64 K_s kernel (and slice padding of k)
+constexpr int kGT = 64;     // tile edge of the float64 K_s kernel
 constexpr int kGK = 16;     // its depth per stage
 
 __global__ void __launch_bounds__(256) row_norms_kernel(const float* X, int64_t rows,
@@ -89,32 +88,6 @@ __global__ void __launch_bounds__(256) reduce_rows_kernel(const float* part, int
     out[b * ldo + c] = f;
 }
 
-__global__ void __launch_bounds__(256) reduce_scale_kernel(const float* part, int slices,
-                                                           int64_t k, int64_t k_pad,
-                                                           int64_t cols, const float* Dk,
-                                                           float* W1) {
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= k * cols) return;
-    const int64_t i = e / cols;
-    float f = 0.f;
-    for (int sl = 0; sl < slices; ++sl) f += part[(int64_t)sl * k_pad * cols + e];
-    W1[e] = Dk[i] * f;
-}
-
-// alpha[r[i], j] += coef * H[i, j] for i < rows, j < l (the fixed-block
-// update of Algorithm 1 step 5; the rows r are distinct, so no two threads
-// touch one element).
-__global__ void __launch_bounds__(256) scatter_add_rows_kernel(const float* H, int64_t ldh,
-                                                               int64_t rows, int64_t l,
-                                                               const int64_t* r, float* alpha,
-                                                               int64_t lda, float coef) {
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= rows * l) return;
-    const int64_t i = e / l;
-    const int64_t j = e - i * l;
-    alpha[r[i] * lda + j] += coef * H[i * ldh + j];
-}
-
 // K_s[i, j] = k(x_ri, x_rj) in float64 from direct coordinate differences.
 __global__ void __launch_bounds__(256) subsample_kernel_f64(const float* Xs, int64_t s,
                                                             int64_t d, int kind, double bw,
@@ -167,24 +140,16 @@ __global__ void __launch_bounds__(256) subsample_kernel_f64(const float* Xs, int
     }
 }
 
-// V[i, j] = Z[i, k - j] (top-k eigenvectors in descending order, float32) and
-// kp_diag[i] = 1 - sum_{j<k} (sigma_j - sigma_k) Z[i, k-j]^2: the adapted
-// kernel k_G(x_ri, x_ri) at each subsample point.
+// V[i, j] = Z[i + (col0 + j col_step) ldz]: the top-k eigenvectors in
+// descending order of their eigenvalues, float32, row-major.
 __global__ void __launch_bounds__(256) extract_eigvecs_kernel(const double* Z, int64_t ldz,
                                                               int64_t col0, int64_t col_step,
-                                                              int64_t s, int64_t k,
-                                                              const double* sig, float* V,
-                                                              int64_t ldv, double* kp_diag) {
+                                                              int64_t s, int64_t k, float* V,
+                                                              int64_t ldv) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= s) return;
-    double acc = 0.0;
-    for (int64_t j = 0; j < k; ++j) {
-        const double z = Z[i + (col0 + j * col_step) * ldz];
-        V[i * ldv + j] = (float)z;
-        acc += (sig[j] - sig[k]) * z * z;
-    }
+    for (int64_t j = 0; j < k; ++j) V[i * ldv + j] = (float)Z[i + (col0 + j * col_step) * ldz];
     for (int64_t j = k; j < ldv; ++j) V[i * ldv + j] = 0.f;
-    kp_diag[i] = 1.0 - acc;
 }
 
 __global__ void __launch_bounds__(256) fill_kernel(float* p, int64_t count, float v) {
@@ -233,22 +198,6 @@ hipError_t launch_reduce_rows(const float* part, int slices, int64_t rows_pad, i
     return hipGetLastError();
 }
 
-hipError_t launch_reduce_scale(const float* part, int slices, int64_t k, int64_t cols_pad,
-                               const float* Dk, float* W1, hipStream_t st) {
-    hipLaunchKernelGGL(reduce_scale_kernel, dim3(blocks_for(k * cols_pad)), dim3(256), 0, st,
-                       part, slices, k, round_up(k, kGT), cols_pad, Dk, W1);
-    return hipGetLastError();
-}
-
-hipError_t launch_scatter_add_rows(const float* H, int64_t ldh, int64_t rows, int64_t l,
-                                   const int64_t* r, float* alpha, int64_t lda, float coef,
-                                   hipStream_t st) {
-    if (rows <= 0 || l <= 0) return hipSuccess;
-    hipLaunchKernelGGL(scatter_add_rows_kernel, dim3(blocks_for(rows * l)), dim3(256), 0, st, H,
-                       ldh, rows, l, r, alpha, lda, coef);
-    return hipGetLastError();
-}
-
 hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d, int kind,
                                        double bandwidth, double* Ks, hipStream_t st) {
     dim3 grid((unsigned)ceil_div(s, kGT), (unsigned)ceil_div(s, kGT));
@@ -258,10 +207,9 @@ hipError_t launch_subsample_kernel_f64(const float* Xs, int64_t s, int64_t d, in
 }
 
 hipError_t launch_extract_eigvecs(const double* Z, int64_t ldz, int64_t col0, int64_t col_step,
-                                  int64_t s, int64_t k, const double* sigma_desc_dev, float* V,
-                                  int64_t ldv, double* kp_diag, hipStream_t st) {
+                                  int64_t s, int64_t k, float* V, int64_t ldv, hipStream_t st) {
     hipLaunchKernelGGL(extract_eigvecs_kernel, dim3(blocks_for(s)), dim3(256), 0, st, Z, ldz,
-                       col0, col_step, s, k, sigma_desc_dev, V, ldv, kp_diag);
+                       col0, col_step, s, k, V, ldv);
     return hipGetLastError();
 }
 

@@ -286,7 +286,7 @@ __device__ __forceinline__ void kmv_body_staged(const KmvArgs& p) {
             // W fragments of the next step in flight during this step's MFMAs
             if (active) {
                 const __amdgpu_buffer_rsrc_t wrs =
-                    make_rsrc(p.W + c0 * p.ldw, (int64_t)kSBN * p.ldw * 4);
+                    make_rsrc(p.W + c0 * p.ldw, (int64_t)kSBN * p.ldw * 4 + kWeightTail);
                 float acur[LTW], anxt[LTW];
                 load_w<LTW>(wrs, w_voff, w_soff(gj, 0), acur);
                 for (int jt = gj; jt < kSCSub; jt += p.wj) {
@@ -488,20 +488,23 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     const int qst_col = 4 * qst_qq;
     const int qst_voff = qst_row * (int)p.ldq * 4 + 16 * qst_qq;
     const int qst_lds = qst_row * kRF + ((qst_qq ^ (qst_row & 15)) << 2);
-    const int qst_step = kRowStep * (int)p.ldq * 4;   // kRowStep rows further (soffset)
+    const int qst_step = kRowStep * (int)p.ldq * 4;   // kRowStep rows further
     // Every load is issued on every path (out-of-range ones at kOOB, which
     // read zeros without touching memory), so that the number of loads in
     // flight is the same on all paths and the compiler's wait counts stay
-    // exact instead of draining the queue.
+    // exact instead of draining the queue. The whole row offset goes in
+    // voffset: the descriptor's range check sees voffset only, so a row
+    // past the tile's last one (a ragged last query tile) reads zero
+    // instead of memory beyond the caller's rows.
     float4 qstage[2];
     auto qload = [&](int part, int bi, bool valid) {
         const int f0 = bi * kRF;
-        const int voff = valid && f0 + qst_col < d ? qst_voff : kOOB;
+        const bool ok = valid && f0 + qst_col < d;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
             qstage[i] = __builtin_bit_cast(
                 float4, __builtin_amdgcn_raw_buffer_load_b128(
-                            qrs, voff, f0 * 4 + (2 * part + i) * qst_step, 0));
+                            qrs, ok ? qst_voff + (2 * part + i) * qst_step : kOOB, f0 * 4, 0));
     };
     auto qwrite = [&](int part, int buf) {
 #pragma unroll
@@ -516,7 +519,7 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     // MFMA pairs feature 4q4 + i of both sides, so every feature is
     // contracted exactly once.
     const int c_voff = ((ct_s * 32 + (lane & 15)) * (int)p.ldc + 4 * q4) * 4;
-    const int c_blk = 16 * (int)p.ldc * 4;   // second centre block (soffset)
+    const int c_blk = 16 * (int)p.ldc * 4;   // second centre block, 16 rows on
     float4 cring[kRP][2];
 #pragma unroll
     for (int c = 0; c < kRP; ++c)
@@ -525,13 +528,16 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         const int64_t c0 = cb + t * kBN;
         return make_rsrc(p.C + c0 * p.ldc, ((ce - c0 - 1) * p.ldc + p.d) * 4);
     };
+    // (row offsets in voffset, as for the queries: rows past the split's
+    // end, in its ragged last tile, read zero)
     auto cload = [&](__amdgpu_buffer_rsrc_t crs, int ch, bool valid, float4* dst) {
         const int f0 = ch * kRDC;
-        const int voff = valid && f0 + 4 * q4 < d ? c_voff : kOOB;
+        const bool ok = valid && f0 + 4 * q4 < d;
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
             dst[cb] = __builtin_bit_cast(
-                float4, __builtin_amdgcn_raw_buffer_load_b128(crs, voff, f0 * 4 + cb * c_blk, 0));
+                float4, __builtin_amdgcn_raw_buffer_load_b128(crs, ok ? c_voff + cb * c_blk : kOOB,
+                                                              f0 * 4, 0));
     };
 
     // B operand (queries) from LDS: quad 4c + q4 of row 16qb + lane%16
@@ -559,9 +565,13 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     auto w_soff = [&](int jt, int v) { return (jt * 32 + ((v >> 2) << 3) + (v & 3)) * ldw4; };
     constexpr int PD = LTW <= 2 ? 16 : 2;
     float wbuf[PD][LTW];
+    // The weight rows of a k-step sit in soffset, which the range check does
+    // not see; the descriptor spans the whole padded tile (kBN rows and the
+    // 16-byte tail every weight matrix carries), which the caller's weights
+    // fill with zeros past their last row, so every load stays inside it.
     auto w_rsrc = [&](int64_t t) {
         const int64_t c0 = cb + t * kBN;
-        return make_rsrc(p.W + c0 * p.ldw, min((int64_t)kBN, ce - c0) * p.ldw * 4);
+        return make_rsrc(p.W + c0 * p.ldw, (int64_t)kBN * p.ldw * 4 + kWeightTail);
     };
     // After the last batch of a tile: kernel values (in accumulator order,
     // which is the operand order of the second product), then

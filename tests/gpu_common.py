@@ -7,6 +7,21 @@ import oracle
 
 TOL_STEP = 1e-4      # relative Frobenius error after one step
 TOL_EPOCH = 1e-3     # relative Frobenius error after one epoch
+# Setup scalars (sigma, beta, m*): float64 on both sides. The device forms
+# K_s from direct coordinate differences, the oracle from the expansion
+# with exact same-point distances, so the two K_s agree to ~1e-15; the
+# eigenpairs come from different float64 solvers (the device's subspace
+# iteration stops at a residual of 1e-11 sigma_1), and beta is a max over
+# the subsample of a sum formed from the float64 eigenvectors on both sides.
+SETUP_RTOL = 1e-9
+
+
+def bw32(bw):
+    """The bandwidth as the library receives it: the C ABI takes it as a
+    float32, and setup and step use exactly that value, so the oracle is
+    handed the same number (0.9 in float32 is 0.9 - 2.4e-8, which moves K_s
+    by ~5e-8)."""
+    return float(np.float32(bw))
 
 
 def rel(a, b):

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_common import Gpu, TOL_STEP, rel
+from gpu_common import Gpu, SETUP_RTOL, TOL_STEP, rel
 
 
 def _problem(n=3000, d=24, l=5, seed=11):
@@ -31,8 +31,8 @@ def test_set_rank_matches_fresh_oracle_setup():
             info = ep.ep_get_info(g.ctx)
             st = oracle.with_rank(big, k)
             assert info.k == k and info.m == st.m
-            assert info.beta == pytest.approx(st.beta, rel=1e-6)
-            assert info.m_star == pytest.approx(st.m_star, rel=1e-6)
+            assert info.beta == pytest.approx(st.beta, rel=SETUP_RTOL)
+            assert info.m_star == pytest.approx(st.m_star, rel=SETUP_RTOL)
             t = rng.choice(n, 150, replace=False)
             a1_o, F_o = oracle.step(st, a0, t, Y[t])
             g.set_alpha(a0)
@@ -64,7 +64,7 @@ def test_adapt_picks_the_eq7_rank():
             assert info.k == k_o, (m_G, info.k, k_o)
             assert info.m == min(n, m_G)
             st = oracle.with_rank(big, k_o)
-            assert info.accel == pytest.approx(oracle.acceleration(st, min(n, m_G)), rel=1e-6)
+            assert info.accel == pytest.approx(oracle.acceleration(st, min(n, m_G)), rel=SETUP_RTOL)
             t = rng.choice(n, info.m, replace=False)
             a1_o, F_o = oracle.step(st, a0, t, Y[t])
             g.set_alpha(a0)

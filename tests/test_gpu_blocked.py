@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import Gpu, TOL_EPOCH, TOL_STEP, kernel_id, rel
+from gpu_common import Gpu, TOL_EPOCH, TOL_STEP, bw32, kernel_id, rel
 
 CASES = [
     # kernel, n, d, l, s, k, m, bw          (d % 4 == 0: the blocked form applies)
@@ -44,6 +44,7 @@ def _kblock_launches(g, fn):
 @pytest.mark.parametrize("case", CASES, ids=[f"{c[0][:3]}-n{c[1]}-d{c[2]}-l{c[3]}-m{c[6]}" for c in CASES])
 def test_blocked_step_and_predict(case, block_bytes):
     kernel, n, d, l, s, k, m, bw = case
+    bw = bw32(bw)
     X, Y, a0, rng = _problem(n, d, l, 3)
     r = rng.choice(n, s, replace=False)
     t = rng.choice(n, m, replace=False).astype(np.int64)

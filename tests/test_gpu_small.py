@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_common import Gpu, TOL_STEP, TOL_EPOCH, kernel_id, lowrank, rel
+from gpu_common import Gpu, SETUP_RTOL, TOL_STEP, TOL_EPOCH, bw32, kernel_id, lowrank, rel
 
 CASES = [
     # kernel, n, d, l, s, k, m, bw
@@ -51,6 +51,7 @@ def _batch(rng, n, r, m):
 @pytest.mark.parametrize("case", CASES, ids=[f"{c[0][:3]}-n{c[1]}-d{c[2]}-l{c[3]}-s{c[4]}-k{c[5]}-m{c[6]}" for c in CASES])
 def test_one_step_setup_predict(case):
     kernel, n, d, l, s, k, m, bw = case
+    bw = bw32(bw)
     X, Y, a0, rng = _problem(n, d, l, 1)
     r = rng.choice(n, s, replace=False)
     t = _batch(rng, n, r, m)
@@ -61,15 +62,13 @@ def test_one_step_setup_predict(case):
     with Gpu(X, l, kernel, bw, s, k, r) as g:
         info = g.info
         assert info.m == st.m
-        # setup is float64 on both sides; the oracle's distance expansion
-        # leaves up to ~1e-8 on the Laplacian diagonal (square root of
-        # rounding noise), so setup scalars are compared at 1e-6
-        assert info.m_star == pytest.approx(st.m_star, rel=1e-6)
-        assert info.beta == pytest.approx(st.beta, rel=1e-6, abs=1e-9)
-        assert info.sigma_k1 == pytest.approx(st.sigma[k], rel=1e-6)
+        # setup is float64 on both sides (SETUP_RTOL)
+        assert info.m_star == pytest.approx(st.m_star, rel=SETUP_RTOL)
+        assert info.beta == pytest.approx(st.beta, rel=SETUP_RTOL)
+        assert info.sigma_k1 == pytest.approx(st.sigma[k], rel=SETUP_RTOL)
         sigma, D, V, r_back = g.preconditioner()
         np.testing.assert_array_equal(r_back, r)
-        np.testing.assert_allclose(sigma, st.sigma, rtol=1e-6)
+        np.testing.assert_allclose(sigma, st.sigma, rtol=SETUP_RTOL)
         if k:
             assert rel(lowrank(V, D), lowrank(st.V, st.D)) < 1e-5
         g.set_alpha(a0)
@@ -97,7 +96,7 @@ EDGES = [
 @pytest.mark.gpu
 @pytest.mark.parametrize("n,d,kernel", EDGES, ids=[f"n{c[0]}-d{c[1]}-{c[2][:3]}" for c in EDGES])
 def test_feature_and_tile_edges(n, d, kernel):
-    l, s, k, m, bw = 5, 60, 4, 70, 1.3
+    l, s, k, m, bw = 5, 60, 4, 70, bw32(1.3)
     X, Y, a0, rng = _problem(n, d, l, 5)
     r = rng.choice(n, s, replace=False)
     t = _batch(rng, n, r, m)
@@ -180,7 +179,7 @@ def test_predict_over_several_row_chunks(kernel):
     with Gpu(X, l, kernel, 1.1, 50, 5, r) as g:
         g.set_alpha(a)
         P = g.predict(Z)
-    P_o = oracle.predict(X, a.astype(np.float64), Z, kernel_id(kernel), 1.1)
+    P_o = oracle.predict(X, a.astype(np.float64), Z, kernel_id(kernel), bw32(1.1))
     assert rel(P, P_o) < TOL_STEP
     for z0 in (0, 32767, 32768, 65535, 65536, 69999):   # rows at the chunk seams
         assert np.allclose(P[z0], P_o[z0], rtol=1e-4, atol=1e-4 * np.abs(P_o).max())
