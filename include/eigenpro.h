@@ -196,6 +196,25 @@ int ep_step(ep_ctx* ctx, const int64_t* t, int64_t m, const float* y_b,
  */
 int ep_predict(ep_ctx* ctx, const float* Z, int64_t n_z, float* out);
 
+/*
+ * ep_predict_noalloc — ep_predict for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. Same arguments and result (up to float32 summation
+ * order); it calls no allocating routine. Its scratch (the row norms of a
+ * chunk of Z and the partial sums of the fused pass) is a 64 MiB array that
+ * the library holds once per device for the life of the process, looked up
+ * when the first context is created on that device. Z is processed in
+ * chunks sized to fit it; always the fused form (ep_set_contraction does
+ * not apply).
+ * Concurrency: every call on one device shares that device's scratch, so
+ * calls that overlap on one GPU (two streams, two threads, two contexts)
+ * race; serialise them. The scratch keeps the last call's contents; nothing
+ * in it needs to start at zero.
+ * Errors: EP_EINVAL (NULL Z / out, n_z < 0, or l so large that one 64-row
+ * chunk's partial sums exceed the scratch: l > 262143), EP_EDEVICE.
+ */
+int ep_predict_noalloc(ep_ctx* ctx, const float* Z, int64_t n_z, float* out);
+
 /* alpha as a dense n x l float32 device matrix (copy out / copy in).
  * Asynchronous on the context stream. */
 int ep_get_alpha(ep_ctx* ctx, float* out);

@@ -83,6 +83,7 @@ def _load():
                            ctypes.POINTER(EpInfo)]),
         "ep_step": (I, [P, P, I64, P, P]),
         "ep_predict": (I, [P, P, I64, P]),
+        "ep_predict_noalloc": (I, [P, P, I64, P]),
         "ep_get_alpha": (I, [P, P]),
         "ep_set_alpha": (I, [P, P]),
         "ep_get_preconditioner": (I, [P, P, P, P, P]),
@@ -229,6 +230,12 @@ def ep_step(ctx, t, m, y_b, f_out=None):
 def ep_predict(ctx, Z, n_z, out):
     torch = _torch()
     return _check(_lib.ep_predict(ctx, _ptr(Z, torch.float32), n_z, _ptr(out, torch.float32)))
+
+
+def ep_predict_noalloc(ctx, Z, n_z, out):
+    torch = _torch()
+    return _check(_lib.ep_predict_noalloc(ctx, _ptr(Z, torch.float32), n_z,
+                                          _ptr(out, torch.float32)))
 
 
 def ep_get_alpha(ctx, out):

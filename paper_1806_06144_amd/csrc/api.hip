@@ -9,6 +9,8 @@
 
 #include <algorithm>
 #include <chrono>
+#include <map>
+#include <mutex>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -48,8 +50,43 @@ uint64_t splitmix64(uint64_t& x) {
 
 }  // namespace
 
+namespace {
+
+// Scratch of ep_predict_noalloc: the row norms of a chunk of query rows
+// followed by the partial sums of its fused pass. One copy lives on every
+// device the library runs on (a file-scope device array, held until the
+// process ends). In host code `scratch` names a host-side stand-in, not the
+// device copy: its device address is looked up once per device
+// (hipGetSymbolAddress, with that device current, when the first context is
+// created there) and only that address is ever handed to kernels.
+constexpr size_t kScratchFloats = size_t(16) << 20;     // 64 MiB
+__device__ __align__(256) float scratch[kScratchFloats];
+
+std::mutex g_scratch_mu;
+std::map<int, float*> g_scratch_dev;    // device -> address of its scratch
+
+// Address of the current device's scratch (looked up on first use).
+int scratch_of_device(int dev, float** out) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    auto it = g_scratch_dev.find(dev);
+    if (it != g_scratch_dev.end()) {
+        *out = it->second;
+        return EP_OK;
+    }
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+        return fail(EP_EDEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_dev[dev] = static_cast<float*>(ptr);
+    *out = static_cast<float*>(ptr);
+    return EP_OK;
+}
+
+}  // namespace
+
 struct ep_ctx {
     int device = 0;
+    float* scratch = nullptr;           // this device's scratch (ep_predict_noalloc)
     hipStream_t stream = nullptr;
     const float* X = nullptr;
     int64_t n = 0, d = 0, l = 0, s = 0, k = 0;
@@ -717,6 +754,10 @@ int create(ep_ctx** out, const float* X, int64_t n, int64_t d, int64_t l, int ke
         delete c;
         return fail(EP_EDEVICE, "no HIP device");
     }
+    if (int rc = scratch_of_device(c->device, &c->scratch)) {
+        delete c;
+        return rc;
+    }
     c->stream = static_cast<hipStream_t>(hip_stream);
     c->X = X;
     c->n = n;
@@ -849,6 +890,74 @@ int ep_predict(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
         if (rc) return rc;
         HIP_TRY(launch_reduce_rows(c->part.as<float>(), slices, rows_pad, c->l_pad, nz, c->l,
                                    out + z0 * c->l, c->l, st));
+    }
+    return EP_OK;
+}
+
+int ep_predict_noalloc(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
+    g_err.clear();
+    if (!c) return fail(EP_EINVAL, "ctx is NULL");
+    if (n_z < 0) return fail(EP_EINVAL, "n_z < 0");
+    if (n_z == 0) return EP_OK;
+    if (!Z || !out) return fail(EP_EINVAL, "Z and out must be device pointers");
+    if (!c->scratch) return fail(EP_EDEVICE, "no scratch address for this device");
+    DeviceGuard dg(c->device);
+    hipStream_t st = c->stream;
+    const int64_t L = c->l_pad;
+    // Chunks of tq query tiles: the fused pass's partial slices (slices x
+    // 64 tq x L floats) and the chunk's row norms (64 tq floats) must fit
+    // the scratch. The slice budget per chunk is what is left after the
+    // norms; tq is halved until the pass's plan fits it.
+    const int64_t cap = (int64_t)kScratchFloats;
+    if (kBM + (int64_t)kBM * L > cap)
+        return fail(EP_EINVAL,
+                    "ep_predict_noalloc: %lld label columns exceed the %zu-float scratch "
+                    "(at most %lld)", (long long)c->l,
+                    kScratchFloats, (long long)((cap - kBM) / kBM));
+    for (int64_t z0 = 0; z0 < n_z;) {
+        int64_t tq = std::min<int64_t>(ceil_div(n_z - z0, kBM), 512);
+        tq = std::max<int64_t>(1, std::min<int64_t>(tq, (cap - kBM) / ((int64_t)kBM * (L + 1))));
+        KmvPlan plan{};
+        int64_t nq = 0, rows_pad = 0;
+        for (;; tq /= 2) {
+            nq = std::min<int64_t>(n_z - z0, tq * kBM);
+            rows_pad = round_up(nq, kBM);
+            const int64_t max_sl = (cap - rows_pad) / (rows_pad * L);
+            plan = kmv_plan(nq, c->n, c->d, L, c->kind, (int)std::min<int64_t>(max_sl, 256));
+            if (max_sl >= 1 && plan.slices() <= max_sl) break;
+            if (tq == 1)
+                return fail(EP_EINVAL,
+                            "ep_predict_noalloc: the fused pass over %lld centres needs more "
+                            "partial sums than the %zu-float scratch holds",
+                            (long long)c->n, kScratchFloats);
+        }
+        float* zn = c->scratch;
+        float* part = c->scratch + rows_pad;
+        const float* Zc = Z + z0 * c->d;
+        HIP_TRY(launch_row_norms(Zc, nq, c->d, c->d, zn, st));
+        KmvArgs a{};
+        a.Q = Zc;
+        a.ldq = c->d;
+        a.qn = zn;
+        a.qid = nullptr;
+        a.nq = nq;
+        a.C = c->X;
+        a.ldc = c->d;
+        a.cn = c->norms.as<float>();
+        a.cid = nullptr;
+        a.nc = c->n;
+        a.d = c->d;
+        a.W = c->alpha.as<float>();
+        a.ldw = L;
+        a.lt = (int)(L / kTile);
+        a.out = part;
+        a.out_rows = rows_pad;
+        a.kind = c->kind;
+        a.scale = c->scale;
+        HIP_TRY(kmv_launch(a, plan, st, false));
+        HIP_TRY(launch_reduce_rows(part, plan.slices(), rows_pad, L, nq, c->l, out + z0 * c->l,
+                                   c->l, st));
+        z0 += nq;
     }
     return EP_OK;
 }
