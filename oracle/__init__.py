@@ -15,6 +15,8 @@ from .eigenpro import (
     OracleState,
     sq_dist,
     kernel_matrix,
+    top_eigenpairs,
+    DENSE_EIG_MAX_S,
     setup,
     step_coefficient,
     beta_closed_form,
@@ -34,6 +36,8 @@ __all__ = [
     "OracleState",
     "sq_dist",
     "kernel_matrix",
+    "top_eigenpairs",
+    "DENSE_EIG_MAX_S",
     "setup",
     "step_coefficient",
     "beta_closed_form",

@@ -12,6 +12,8 @@ What each function follows
 --------------------------
 kernel_matrix      Appendix B: Gaussian exp(-|x-z|^2 / (2 sigma^2)) and
                    Laplacian exp(-|x-z| / sigma).
+top_eigenpairs     the top q eigenpairs of K_s by a library routine (LAPACK
+                   dense, or ARPACK Lanczos for large s).
 setup              Algorithm 1 (initialisation: subsample r, top eigensystem
                    of K_s); Section 4 (Nystrom extension: lambda_i ~ sigma_i/s,
                    D = Sigma^-1 (1 - sigma_q Sigma^-1)); Section 3, Step 2
@@ -68,6 +70,7 @@ from dataclasses import dataclass
 
 import numpy as np
 import scipy.linalg
+import scipy.sparse.linalg
 
 GAUSSIAN = 0
 LAPLACIAN = 1
@@ -165,7 +168,38 @@ def beta_closed_form(sigma, V):
     return float(np.max(1.0 - (V * V) @ w))
 
 
-def setup(X, kernel, bandwidth, s, k, sub_idx):
+# subsample sizes up to which top_eigenpairs uses the dense routine
+DENSE_EIG_MAX_S = 4000
+
+
+def top_eigenpairs(K, q, method="auto"):
+    """The q largest eigenvalues of the symmetric matrix K (descending) and
+    their unit eigenvectors, by a library routine:
+
+    dense    LAPACK's symmetric eigensolver (scipy.linalg.eigh) restricted to
+             the top q; its reduction to tridiagonal form costs O(s^3) and
+             takes minutes at s = 12000-20000;
+    lanczos  ARPACK's implicitly restarted Lanczos iteration
+             (scipy.sparse.linalg.eigsh) on K, which needs only products
+             K v; a fixed seeded start vector makes it deterministic;
+    auto     dense up to DENSE_EIG_MAX_S rows, else lanczos.
+    """
+    s = K.shape[0]
+    if method == "auto":
+        method = "dense" if s <= DENSE_EIG_MAX_S or q >= s else "lanczos"
+    if method == "dense":
+        w, U = scipy.linalg.eigh(K, subset_by_index=[s - q, s - 1])
+    elif method == "lanczos":
+        v0 = np.random.default_rng(12345).standard_normal(s)
+        w, U = scipy.sparse.linalg.eigsh(K, k=q, which="LA", tol=1e-14, v0=v0,
+                                         ncv=min(s, max(2 * q + 1, q + 64)))
+    else:
+        raise ValueError(f"unknown eigen method {method!r}")
+    order = np.argsort(w)[::-1]
+    return w[order].copy(), U[:, order].copy()
+
+
+def setup(X, kernel, bandwidth, s, k, sub_idx, eig="auto"):
     """Algorithm 1 initialisation + Section 4 + Section 3 Steps 2-3."""
     n = X.shape[0]
     r = np.asarray(sub_idx, dtype=np.int64)
@@ -173,10 +207,8 @@ def setup(X, kernel, bandwidth, s, k, sub_idx):
         raise ValueError("need 0 <= k < s <= n and s subsample indices")
     Xs = _f64(X[r])
     Ks = kernel_matrix(Xs, Xs, kernel, bandwidth, r, r)
-    # top k+1 eigenpairs of K_s (ascending from LAPACK, reversed)
-    w, U = scipy.linalg.eigh(Ks, subset_by_index=[s - k - 1, s - 1])
-    sigma = w[::-1].copy()
-    U = U[:, ::-1]
+    # top k+1 eigenpairs of K_s
+    sigma, U = top_eigenpairs(Ks, k + 1, eig)
     V = U[:, :k].copy()
     D = (1.0 - sigma[k] / sigma[:k]) / sigma[:k]
     beta = beta_closed_form(sigma, V)

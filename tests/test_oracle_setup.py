@@ -115,3 +115,34 @@ def test_eigenvector_sign_invariance():
     st = oracle.setup(X, oracle.LAPLACIAN, 1.0, 45, 6, np.arange(45))
     flipped = st.V * np.where(np.arange(6) % 2 == 0, -1.0, 1.0)
     assert oracle.beta_closed_form(st.sigma, flipped) == pytest.approx(st.beta, abs=1e-15)
+
+
+@pytest.mark.parametrize("kernel,bw", [(oracle.GAUSSIAN, 15.0), (oracle.LAPLACIAN, 10.0)])
+def test_lanczos_route_equals_dense_eigh(kernel, bw):
+    """The two library routes of top_eigenpairs give the same eigensystem on a
+    K_s with the flat bulk of the workloads (rows from the TIMIT-shaped law:
+    one large eigenvalue, then near-equal ones around sigma_{k+1})."""
+    rng = np.random.default_rng(21)
+    X = rng.standard_normal((1500, 440))
+    Ks = kmat(X, X, kernel, bw)
+    q = 121
+    wd, Ud = oracle.top_eigenpairs(Ks, q, "dense")
+    wl, Ul = oracle.top_eigenpairs(Ks, q, "lanczos")
+    np.testing.assert_allclose(wl, wd, rtol=1e-12)
+    assert np.all(np.diff(wl) <= 0)
+    # the bulk really is flat: sigma_q and sigma_{q-1} within 1 %
+    assert wd[q - 2] / wd[q - 1] < 1.01
+    # same spectral projector onto the top q - 1 (eigenvector signs and
+    # rotations inside near-degenerate pairs do not matter there)
+    D = 1.0 / wd[:q - 1]
+    Pd = (Ud[:, :q - 1] * D) @ Ud[:, :q - 1].T
+    Pl = (Ul[:, :q - 1] * D) @ Ul[:, :q - 1].T
+    assert np.linalg.norm(Pl - Pd) / np.linalg.norm(Pd) < 1e-9
+    res = Ks @ Ul - Ul * wl
+    assert np.linalg.norm(res) <= 1e-10 * np.linalg.norm(Ks)
+    # and the setup built on either route agrees
+    r = np.arange(1500)
+    st_d = oracle.setup(X, kernel, bw, 1500, q - 1, r, eig="dense")
+    st_l = oracle.setup(X, kernel, bw, 1500, q - 1, r, eig="lanczos")
+    assert st_l.beta == pytest.approx(st_d.beta, rel=1e-11)
+    assert st_l.m_star == pytest.approx(st_d.m_star, rel=1e-11)
