@@ -74,53 +74,133 @@ def measured_traffic(workload, kernel="kmv_kernel"):
     return entry.get("bytes_per_launch")
 
 
-def cpu_baseline(X, alpha_host, cfg, target_s=20.0):
-    """The fp64 oracle's kernel-block contraction F = K(X_t, X) alpha (the
-    dominant part of a step) on a bounded sample of batch rows against all n
-    centres, scaled to kernel entries per second."""
-    import oracle
+def host_cores():
+    """(physical cores by lscpu, CPUs this process may run on, the
+    OMP_NUM_THREADS cap or None)."""
+    import subprocess
+    phys = None
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:
-        cores = os.cpu_count() or 1
-    rng = np.random.default_rng(123)
-    kid = {"gaussian": oracle.GAUSSIAN, "laplacian": oracle.LAPLACIAN}[cfg.kernel]
-    def timed(rows):
-        Q = X[rng.choice(X.shape[0], rows, replace=False)]
-        t0 = time.perf_counter()
-        oracle.predict(X, alpha_host, Q, kid, cfg.bandwidth)
-        return time.perf_counter() - t0
+        out = subprocess.run(["lscpu", "-p=SOCKET,CORE"], capture_output=True, text=True,
+                             timeout=20).stdout
+        pairs = {line.strip() for line in out.splitlines() if line and not line.startswith("#")}
+        phys = len(pairs) or None
+    except (OSError, subprocess.SubprocessError):
+        phys = None
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS")
+    omp = int(omp) if omp and omp.isdigit() else None
+    return phys, nproc, omp
 
-    # Each call pays a per-centre cost (converting and norming X block by
-    # block) plus a per-row cost, so time grows more slowly than the row
-    # count; scaling the rows by target/time therefore stays below the
-    # target, and two rescales bring the reported call near it.
-    rows = 64
-    dt = timed(rows)
-    for _ in range(2):
+
+def timing_state(X, cfg, seed=0):
+    """An oracle state for timing oracle.step on the workload: the
+    workload's subsample and shapes, with a seeded orthonormal s x k basis
+    and a decreasing spectrum standing in for the eigensystem (the step's
+    arithmetic, and so its time, does not depend on their values; the
+    oracle's own eigensolve is a setup cost, not part of a step)."""
+    import oracle
+    import synth
+    n = X.shape[0]
+    r = synth.subsample_indices(cfg, seed, n=n)
+    rng = np.random.default_rng(seed + 99)
+    V = np.linalg.qr(rng.standard_normal((cfg.s, cfg.k)))[0] if cfg.k else np.zeros((cfg.s, 0))
+    sigma = cfg.s * 0.5 * 0.98 ** np.arange(cfg.k + 1)
+    D = (1.0 - sigma[cfg.k] / sigma[:cfg.k]) / sigma[:cfg.k]
+    beta = oracle.beta_closed_form(sigma, V)
+    lam = sigma[cfg.k] / cfg.s
+    m_star = beta / lam
+    return oracle.OracleState(X, cfg.kernel_id, float(cfg.bandwidth), r,
+                              np.asarray(X[r], dtype=np.float64), sigma, V, D, float(beta),
+                              float(lam), float(m_star), int(min(n, max(1, np.floor(m_star)))))
+
+
+def _timed_rows(fn, n_rows_max, target_s, start=32):
+    """Run fn(rows) with a growing row count until one call takes about
+    target_s; returns (rows, seconds) of the last call. Each call pays a
+    per-centre cost as well as a per-row one, so time grows more slowly
+    than the row count and two rescales bring the call near the target."""
+    rows = min(start, n_rows_max)
+    dt = fn(rows)
+    for _ in range(3):
         if dt >= 0.6 * target_s:
             break
-        grown = int(min(X.shape[0], 20000, rows * target_s / max(dt, 1e-3)))
+        grown = int(min(n_rows_max, rows * target_s / max(dt, 1e-3)))
         if grown <= rows:
             break
         rows = grown
-        dt = timed(rows)
-    rate = rows * X.shape[0] / dt
-    n = X.shape[0]
-    return {
-        "value": rate,
-        "unit": "entries/s",
-        "cores": int(cores),
-        "kind": "oracle",
-        # an epoch evaluates n (n + s) kernel entries (every row against all
-        # centres in step 2 and against the subsample in steps 4-5): the
-        # oracle's epoch at the measured rate, extrapolated, not run
-        "s_per_epoch_extrapolated": n * (n + cfg.s) / rate,
-        "sample": (f"fp64 oracle F = K(X_t, X) alpha for {rows} batch rows against all "
-                   f"{X.shape[0]} centres (d={X.shape[1]}, l={alpha_host.shape[1]}), "
-                   f"{dt:.1f} s"),
-    }
+        dt = fn(rows)
+    return rows, dt
+
+
+def cpu_baseline(X, alpha_host, cfg, m, configs=("tiny", "mnist", "cifar", "timit"),
+                 target_s=8.0):
+    """The float64 oracle timed on the host cores with BLAS pinned to the
+    physical core count (capped by the CPUs and OMP_NUM_THREADS this process
+    may use): a whole oracle.step (Algorithm 1 steps 1-5) on a bounded batch
+    of the headline workload, step 2 alone (F = K(X_t, X) alpha) on it, and
+    a whole step on each other workload, each reported as kernel entries per
+    second (batch rows x n over the call's time)."""
+    import oracle
+    import synth
+    from threadpoolctl import threadpool_limits
+
+    phys, nproc, omp = host_cores()
+    cores = min(x for x in (phys, nproc, omp) if x)
+    rng = np.random.default_rng(123)
+    out = {"unit": "entries/s", "kind": "oracle", "cores": int(cores),
+           "physical_cores": phys, "nproc": nproc, "omp_num_threads": omp}
+    with threadpool_limits(limits=cores):
+        st = timing_state(X, cfg)
+        y_of = lambda t: np.zeros((len(t), alpha_host.shape[1]))
+
+        def whole(rows, st=st, alpha=alpha_host):
+            t = rng.choice(st.n, rows, replace=False)
+            t0 = time.perf_counter()
+            oracle.step(st, alpha, t, y_of(t))
+            return time.perf_counter() - t0
+
+        def step2(rows):
+            Q = X[rng.choice(X.shape[0], rows, replace=False)]
+            t0 = time.perf_counter()
+            oracle.predict(X, alpha_host, Q, cfg.kernel_id, cfg.bandwidth)
+            return time.perf_counter() - t0
+
+        rows, dt = _timed_rows(whole, min(m, X.shape[0]), 2.0 * target_s)
+        n = X.shape[0]
+        out["value"] = rows * n / dt
+        # an epoch is ceil(n/m) steps of m rows; a step's time is close to
+        # linear in its rows (its F and G parts are), so the measured rate
+        # carries over to the full batch
+        out["s_per_epoch_extrapolated"] = -(-n // m) * dt * (m / rows)
+        out["sample"] = (f"oracle.step (Algorithm 1 steps 1-5, float64) on {rows} batch rows of "
+                         f"the {cfg.name}-shaped workload (n={n}, d={X.shape[1]}, l={cfg.l}, "
+                         f"s={cfg.s}, k={cfg.k}): {dt:.1f} s; the eigensystem is a seeded "
+                         f"stand-in (time does not depend on it)")
+        rows2, dt2 = _timed_rows(step2, min(m, X.shape[0]), target_s)
+        out["step2_value"] = rows2 * n / dt2
+        out["step2_sample"] = f"oracle F = K(X_t, X) alpha for {rows2} rows: {dt2:.1f} s"
+        per = []
+        for name in configs:
+            c = synth.get_config(name)
+            Xc = synth.features(c, 0)
+            stc = timing_state(Xc, c)
+            ac = synth.initial_alpha(c.n, c.l, 0)
+
+            def whole_c(rows, stc=stc, ac=ac):
+                t = rng.choice(stc.n, rows, replace=False)
+                t0 = time.perf_counter()
+                oracle.step(stc, ac, t, np.zeros((rows, c.l)))
+                return time.perf_counter() - t0
+
+            rc_, dc_ = _timed_rows(whole_c, min(4096, c.n), target_s / 2)
+            per.append({"workload": name, "n": c.n, "d": c.d, "l": c.l, "s": c.s, "k": c.k,
+                        "batch_rows": rc_, "step_s": dc_, "value": rc_ * c.n / dc_})
+            del Xc, stc, ac
+        out["per_config"] = per
+    return out
 
 
 def study_batch(args):
@@ -591,8 +671,8 @@ def main():
         alpha = torch.empty((n, l), dtype=torch.float32, device=dev)
         ep.ep_get_alpha(ctx, alpha)
         ep.ep_sync(ctx)
-        log("timing the oracle on a bounded sample")
-        cpu = cpu_baseline(X, alpha.cpu().numpy(), cfg)
+        log("timing the oracle on bounded samples")
+        cpu = cpu_baseline(X, alpha.cpu().numpy(), cfg, m)
     ep.ep_destroy(ctx)
 
     traffic = measured_traffic(workload, dom)

@@ -109,32 +109,3 @@ def test_contraction_mode_errors():
             with pytest.raises(ep.EigenProError) as e:
                 ep.ep_set_contraction(g.ctx, mode, nbytes)
             assert e.value.code == ep.EP_EINVAL
-
-
-@pytest.mark.gpu
-@pytest.mark.timeout(900)
-def test_blocked_matches_fused_at_imagenet_shape():
-    """ImageNet-shaped workload at full size, the bench's batch: both forms
-    from the same alpha0; F agrees to float32 summation order, and sampled
-    rows agree with the oracle computed one by one."""
-    cfg = synth.get_config("imagenet")
-    w = synth.make_workload(cfg, 0)
-    kid = kernel_id(cfg.kernel)
-    a0 = synth.initial_alpha(w.n, cfg.l, 0)
-    out = {}
-    for form in ["fused", "blocked"]:
-        with Gpu(w.X, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k, w.r,
-                 contraction=form) as g:
-            m = int(g.info.m)
-            t = synth.epoch_batches(w.n, m, 0)[0]
-            g.set_alpha(a0)
-            F, launches = _kblock_launches(g, lambda: g.step(t, w.y(t)))
-            assert (launches > 0) == (form == "blocked")
-            out[form] = (F, g.alpha(), t)
-    (F1, A1, t), (F2, A2, _) = out["fused"], out["blocked"]
-    assert rel(F2, F1) < 1e-5
-    assert rel(A2 - a0, A1 - a0) < 1e-5
-    rng = np.random.default_rng(11)
-    sample = rng.choice(len(t), 16, replace=False)
-    F_o = oracle.predict(w.X, a0, w.X[t[sample]], kid, cfg.bandwidth)
-    assert rel(F2[sample], F_o) < TOL_STEP
