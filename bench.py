@@ -61,17 +61,25 @@ def kernel_source_sha(kernel="kmv_kernel"):
 
 def measured_traffic(workload, kernel="kmv_kernel"):
     """HBM bytes per launch of the dominant kernel from committed rocprofv3
-    counter runs, if they were taken on the current kernel source."""
+    counter runs, if they were taken on the current kernel source, and where
+    the figure comes from: (bytes or None, provenance dict)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    key = f"{workload} | {kernel}"
+    prov = {"record": "profiles/hbm_traffic.json", "key": key,
+            "kernel_source_sha": kernel_source_sha(kernel),
+            "measured_with": "rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE runs of bench.py "
+                             "(counters calibrated against 1 GiB device copies); not this run"}
     try:
         with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
-        return None
-    entry = rec.get(f"{workload} | {kernel}")
-    if not entry or entry.get("source_sha") != kernel_source_sha(kernel):
-        return None
-    return entry.get("bytes_per_launch")
+        return None, dict(prov, status="no record")
+    entry = rec.get(key)
+    if not entry:
+        return None, dict(prov, status="no record for this workload")
+    if entry.get("source_sha") != prov["kernel_source_sha"]:
+        return None, dict(prov, status=f"record taken on other kernel code ({entry.get('source_sha')})")
+    return entry.get("bytes_per_launch"), dict(prov, status="record matches the kernel code")
 
 
 def host_cores():
@@ -675,7 +683,7 @@ def main():
         cpu = cpu_baseline(X, alpha.cpu().numpy(), cfg, m)
     ep.ep_destroy(ctx)
 
-    traffic = measured_traffic(workload, dom)
+    traffic, traffic_prov = measured_traffic(workload, dom)
     out = {
         "metric": "kernel entries/s (m*n per step)",
         "value": entries / sec_per_step,
@@ -707,6 +715,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
             "traffic": traffic,
+            "traffic_source": traffic_prov,
             "kernel": dom_label,
             "avg_launch_ms": dom_avg_s * 1e3,
             "launches": launches,
