@@ -211,40 +211,70 @@ def cpu_baseline(X, alpha_host, cfg, m, configs=("tiny", "mnist", "cifar", "timi
     return out
 
 
+def _time_steps(ep, torch, ctx, stream, tl, yl):
+    """Median HIP-event time (ms) of ep_step over the given device batches,
+    on the library's stream (torch's current stream here)."""
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(tl) + 1)]
+    evs[0].record(stream)
+    for i, (tb, yb) in enumerate(zip(tl, yl)):
+        ep.ep_step(ctx, tb, tb.shape[0], yb)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return float(np.median([evs[i].elapsed_time(evs[i + 1]) for i in range(len(tl))]))
+
+
 def study_batch(args):
     """Synthetic analogue of the paper's batch-size / GPU-utilisation study
-    (Section 5, Figure 4): time per step against batch size on a
-    TIMIT-shaped problem (n = 1e5, d = 440, l = 144), the resource batch of
-    Section 3 Step 1, the Eq. 7 rank for it, and time per epoch against n at
-    that batch."""
+    (Section 5, Figure 4): time per iteration (a whole ep_step, Algorithm 1
+    steps 1-5) and per step-2 pass against batch size on a TIMIT-shaped
+    problem (n = 1e5, d = 440, l = 144), the resource batch of Section 3
+    Step 1 (the knee of that curve), the Eq. 7 rank for it, and time per
+    epoch against n at that batch."""
     import torch
     import synth
     import paper_1806_06144_amd as ep
     dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
     base = synth.get_config("timit")
     out = []
     cfg = synth.get_config("timit", n=100000, s=4000, k=400)
     X = synth.features(cfg, 0)
+    labels = synth.class_labels(cfg, X, 0)
     Xd = torch.from_numpy(X).to(dev)
     ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
-                            sub_idx=synth.subsample_indices(cfg, 0))
+                            sub_idx=synth.subsample_indices(cfg, 0), stream=stream)
     ms = [2 ** j for j in range(4, 15)]
     t = ep.ep_batch_sweep(ctx, ms, reps=3)
+    alpha0 = torch.zeros((cfg.n, cfg.l), dtype=torch.float32, device=dev)
+    perm = synth.epoch_permutation(cfg.n, 0)
     for m, tm in zip(ms, t):
-        rec = {"study": "time_per_step_vs_batch", "n": cfg.n, "d": cfg.d, "l": cfg.l, "m": m,
-               "fused_pass_ms": tm, "entries_per_s": m * cfg.n / (tm * 1e-3)}
+        # whole iterations on distinct batches of this size, from alpha = 0
+        # each time (the timing does not depend on alpha)
+        reps = 5
+        tl = [torch.from_numpy(perm[(i * m) % cfg.n:(i * m) % cfg.n + m].copy()).to(dev)
+              for i in range(reps)]
+        tl = [x if x.shape[0] == m else torch.from_numpy(perm[:m].copy()).to(dev) for x in tl]
+        yl = [torch.from_numpy(synth.one_hot(labels[x.cpu().numpy()], cfg.l)).to(dev) for x in tl]
+        ep.ep_set_alpha(ctx, alpha0)
+        ep.ep_step(ctx, tl[0], m, yl[0])
+        step_ms = _time_steps(ep, torch, ctx, stream, tl, yl)
+        rec = {"study": "time_per_iteration_vs_batch", "n": cfg.n, "d": cfg.d, "l": cfg.l,
+               "m": m, "step_ms": step_ms, "fused_pass_ms": tm,
+               "entries_per_s": m * cfg.n / (step_ms * 1e-3)}
         out.append(rec)
         log(json.dumps(rec))
+    ep.ep_set_alpha(ctx, alpha0)
     m_C, m_S, m_G = ep.ep_resource_batch(ctx, 0.1)
-    info0 = ep.ep_adapt(ctx, 1)                   # rank of the original kernel's m*
+    m_C2 = ep.ep_resource_batch(ctx, 0.1)[0]
+    _, knee = ep.ep_batch_knee(ms, t, 0.1)
     ep.ep_set_rank(ctx, 0)
     mstar0 = ep.ep_get_info(ctx).m_star
     ad = ep.ep_adapt(ctx, m_G)
-    rec = {"study": "resource_adaptive", "n": cfg.n, "k_max": cfg.k, "m_C": m_C, "m_S": m_S,
-           "m_G": m_G, "chosen_k": ad.k, "m_star_original": mstar0, "m_star_adapted": ad.m_star,
+    rec = {"study": "resource_adaptive", "n": cfg.n, "k_max": cfg.k, "m_C": m_C,
+           "m_C_second_call": m_C2, "knee_of_this_sweep": knee, "m_S": m_S, "m_G": m_G,
+           "chosen_k": ad.k, "m_star_original": mstar0, "m_star_adapted": ad.m_star,
            "beta_adapted": ad.beta, "sigma_1": ad.sigma_1, "sigma_k1": ad.sigma_k1,
            "acceleration": ad.accel, "step_eta": ad.eta}
-    del info0
     out.append(rec)
     log(json.dumps(rec))
     ep.ep_destroy(ctx)
@@ -279,12 +309,93 @@ def study_batch(args):
     return out
 
 
+def _train_to(ep, torch, ctx, Xd, Y, n, m, thr, max_epochs, budget_s, first_epoch=0):
+    """Epochs of Algorithm 1 from alpha = 0 at batch m until the training
+    MSE (mean over points and labels) falls below thr, or a cap; returns
+    (epochs, step seconds, final MSE)."""
+    import synth
+    dev = Xd.device
+    P = torch.empty_like(Y)
+
+    def mse():
+        ep.ep_predict(ctx, Xd, n, P)
+        ep.ep_sync(ctx)
+        return float(((P - Y) ** 2).mean())
+
+    ep.ep_set_alpha(ctx, torch.zeros_like(Y))
+    gpu_s, epochs, err = 0.0, 0, mse()
+    while err >= thr and epochs < max_epochs and gpu_s < budget_s:
+        batches = synth.epoch_batches(n, m, first_epoch + epochs)
+        tl = [torch.from_numpy(b).to(dev) for b in batches]
+        yl = [Y[b] for b in tl]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for tb, yb in zip(tl, yl):
+            ep.ep_step(ctx, tb, tb.shape[0], yb)
+        ep.ep_sync(ctx)
+        gpu_s += time.perf_counter() - t0
+        epochs += 1
+        err = mse()
+    return epochs, gpu_s, err
+
+
 def study_convergence(args):
     """Synthetic analogue of the paper's convergence comparison (Section 5,
     Figure 3): epochs and GPU time to bring the training MSE (mean over
-    points and labels) below a threshold, against batch size, for plain
-    kernel SGD (rank 0, its own optimal step) and EigenPro 2.0 (the Eq. 7
-    rank for the resource batch), on a TIMIT-shaped problem with n = 1e5."""
+    points and labels) below a threshold, against batch size m, for plain
+    kernel SGD (rank 0, its own optimal step) and EigenPro 2.0 with the
+    kernel adapted to the batch (the Eq. 7 rank for m_G = m, the step size
+    of Section 3 Step 3). TIMIT-shaped problem with n = 1e5 and
+    threshold 2e-4 (--study convergence), or the MNIST-shaped workload at
+    its full size with threshold 1e-4 (--study convergence-mnist, the
+    paper's threshold for its MNIST curves)."""
+    import torch
+    import synth
+    import paper_1806_06144_amd as ep
+    dev = torch.device("cuda:0")
+    if args.study == "convergence-mnist":
+        cfg = synth.get_config("mnist", s=4000, k=400)
+        thr, max_epochs, budget_s = 1e-4, 200, 30.0
+    else:
+        cfg = synth.get_config("timit", n=100000, s=4000, k=400)
+        thr, max_epochs, budget_s = 2e-4, 40, 60.0
+    X = synth.features(cfg, 0)
+    labels = synth.class_labels(cfg, X, 0)
+    Xd = torch.from_numpy(X).to(dev)
+    Y = torch.from_numpy(synth.one_hot(labels, cfg.l)).to(dev)
+    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
+                            sub_idx=synth.subsample_indices(cfg, 0))
+    _, _, m_G = ep.ep_resource_batch(ctx, 0.1)
+    k_G = ep.ep_adapt(ctx, m_G).k
+    out = []
+    for method in ("sgd", "eigenpro"):
+        for m in (64, 256, 1024, 4096):
+            if method == "sgd":
+                ep.ep_set_rank(ctx, 0)
+            else:
+                ep.ep_adapt(ctx, m)
+            inf = ep.ep_get_info(ctx)
+            epochs, gpu_s, err = _train_to(ep, torch, ctx, Xd, Y, cfg.n, m, thr, max_epochs,
+                                           budget_s)
+            rec = {"study": "convergence", "workload": cfg.name, "n": cfg.n, "method": method,
+                   "k": inf.k, "m_star": inf.m_star, "m": m, "epochs": epochs,
+                   "step_time_s": gpu_s, "train_mse": err, "threshold": thr,
+                   "converged": err < thr, "m_G": m_G, "k_at_m_G": k_G}
+            out.append(rec)
+            log(json.dumps(rec))
+    ep.ep_destroy(ctx)
+    return out
+
+
+def study_kernels(args):
+    """The paper's remarks on the kernel function (Section 5): with the
+    Laplacian kernel training takes fewer epochs, and its critical batch m*
+    is larger, than with the Gaussian. Same TIMIT-shaped data (n = 1e5,
+    d = 440, l = 144), same bandwidth 15 (Table 5's TIMIT row uses the
+    Laplacian kernel at 15), same subsample; for each kernel: m* at ranks
+    0, 1, 10, 100 and 400 (Section 3 Step 2), and epochs and GPU time to
+    training MSE < 2e-4 for plain kernel SGD at m = 64 and for EigenPro 2.0
+    at m = 4096 with the kernel adapted to that batch (Eq. 7)."""
     import torch
     import synth
     import paper_1806_06144_amd as ep
@@ -294,42 +405,28 @@ def study_convergence(args):
     labels = synth.class_labels(cfg, X, 0)
     Xd = torch.from_numpy(X).to(dev)
     Y = torch.from_numpy(synth.one_hot(labels, cfg.l)).to(dev)
-    ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, cfg.kernel, cfg.bandwidth, cfg.s, cfg.k,
-                            sub_idx=synth.subsample_indices(cfg, 0))
-    _, _, m_G = ep.ep_resource_batch(ctx, 0.1)
-    k_ad = ep.ep_adapt(ctx, m_G).k
-    P = torch.empty_like(Y)
-    thr, max_epochs, budget_s = 2e-4, 40, 60.0
+    r = synth.subsample_indices(cfg, 0)
     out = []
-
-    def mse():
-        ep.ep_predict(ctx, Xd, cfg.n, P)
-        ep.ep_sync(ctx)
-        return float(((P - Y) ** 2).mean())
-
-    for k in (0, k_ad):
-        ep.ep_set_rank(ctx, k)
-        for m in (64, 256, 1024, 4096):
-            ep.ep_set_alpha(ctx, torch.zeros_like(Y))
-            gpu_s, epochs, err = 0.0, 0, mse()
-            while err >= thr and epochs < max_epochs and gpu_s < budget_s:
-                batches = synth.epoch_batches(cfg.n, m, epochs)
-                tl = [torch.from_numpy(b).to(dev) for b in batches]
-                yl = [Y[b] for b in tl]
-                torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                for tb, yb in zip(tl, yl):
-                    ep.ep_step(ctx, tb, tb.shape[0], yb)
-                ep.ep_sync(ctx)
-                gpu_s += time.perf_counter() - t0
-                epochs += 1
-                err = mse()
-            rec = {"study": "convergence", "n": cfg.n, "k": k, "m": m, "epochs": epochs,
-                   "step_time_s": gpu_s, "train_mse": err, "threshold": thr,
-                   "converged": err < thr, "m_G": m_G}
-            out.append(rec)
-            log(json.dumps(rec))
-    ep.ep_destroy(ctx)
+    for kernel in ("gaussian", "laplacian"):
+        ctx, info = ep.ep_setup(Xd, cfg.n, cfg.d, cfg.l, kernel, cfg.bandwidth, cfg.s, cfg.k,
+                                sub_idx=r)
+        mstar = {}
+        for k in (0, 1, 10, 100, 400):
+            ep.ep_set_rank(ctx, k)
+            mstar[str(k)] = ep.ep_get_info(ctx).m_star
+        ep.ep_set_rank(ctx, 0)
+        sgd = _train_to(ep, torch, ctx, Xd, Y, cfg.n, 64, 2e-4, 40, 60.0)
+        ad = ep.ep_adapt(ctx, 4096)
+        epro = _train_to(ep, torch, ctx, Xd, Y, cfg.n, ad.m, 2e-4, 40, 60.0)
+        rec = {"study": "kernel_choice", "kernel": kernel, "bandwidth": cfg.bandwidth,
+               "n": cfg.n, "sigma_1": info.sigma_1, "m_star_by_rank": mstar,
+               "sgd_m": 64, "sgd_epochs": sgd[0], "sgd_step_s": sgd[1], "sgd_mse": sgd[2],
+               "eigenpro_m": ad.m, "eq7_rank": ad.k, "m_star_adapted": ad.m_star,
+               "eigenpro_epochs": epro[0], "eigenpro_step_s": epro[1], "eigenpro_mse": epro[2],
+               "threshold": 2e-4}
+        out.append(rec)
+        log(json.dumps(rec))
+        ep.ep_destroy(ctx)
     return out
 
 
@@ -470,7 +567,8 @@ def main():
                          "WRITE_SIZE; runs with --calibrate-copy) into profiles/hbm_traffic.json "
                          "for the workload named in BENCH_OUT (the JSON line of the counted "
                          "run), and print a summary; no GPU needed")
-    ap.add_argument("--study", choices=["batch", "convergence", "setup"], default=None,
+    ap.add_argument("--study", choices=["batch", "convergence", "convergence-mnist", "kernels",
+                                        "setup"], default=None,
                     help="run a study instead of the benchmark (JSON lines on stdout)")
     args = ap.parse_args()
     if args.traffic_summary:
@@ -487,6 +585,7 @@ def main():
         return
     if args.study:
         fn = {"batch": study_batch, "convergence": study_convergence,
+              "convergence-mnist": study_convergence, "kernels": study_kernels,
               "setup": study_setup}[args.study]
         for rec in fn(args):
             print(json.dumps(rec), flush=True)

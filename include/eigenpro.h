@@ -249,10 +249,21 @@ int ep_get_info(ep_ctx* ctx, ep_info* info);
  *   in ms (host array of count doubles). Synchronises. Errors: EP_EINVAL.
  * ep_resource_batch(ctx, tol, m_C, m_S, m_G): Step 1. m_S = the batch at
  *   which the paper's memory model (d + l + m) n floats fills the device's
- *   memory; m_C = the smallest power-of-two batch (32 .. 32768) whose
- *   measured kernel-entry throughput is within tol of the best, i.e. where
- *   time per step stops being flat; m_G = min(m_C, m_S). Any output may be
- *   NULL. Synchronises. Errors: EP_EINVAL (tol outside (0, 1)).
+ *   memory; m_C = the batch where time per iteration stops being flat
+ *   ((d + l) m_C n ~ the device's parallel capacity): the step-2 pass is
+ *   timed at power-of-two batches 16 .. min(n, 32768), three sweeps of three
+ *   launches each, the median of each batch is kept, and ep_batch_knee
+ *   places the knee; m_G = min(m_C, m_S). Any output may be NULL.
+ *   Synchronises. Errors: EP_EINVAL (tol outside [0, 1)).
+ * ep_batch_knee(ms, ms_per_pass, count, tol, m_C, knee): host only (no
+ *   device work). Fits time(m) = max(t0, a m), flat then linear, to count >= 2
+ *   increasing batch sizes ms and their times by least squares on log time
+ *   (each split of the points into a flat and a linear part fits t0 and a
+ *   as geometric means; the split with the smallest residual wins), and
+ *   returns the knee t0 / a and m_C = the smallest power of two at or above
+ *   (1 - tol) knee, clamped to [ms[0], ms[count-1]]. Either output may be
+ *   NULL. Errors: EP_EINVAL (count < 2, ms not increasing or < 1, a time
+ *   not positive and finite, tol outside [0, 1)).
  */
 int ep_set_rank(ep_ctx* ctx, int64_t k);
 int ep_adapt(ep_ctx* ctx, int64_t m_G, ep_info* info);
@@ -260,6 +271,8 @@ int ep_batch_sweep(ep_ctx* ctx, const int64_t* ms, int count, int reps,
                    double* ms_per_pass);
 int ep_resource_batch(ep_ctx* ctx, double tol, int64_t* m_C, int64_t* m_S,
                       int64_t* m_G);
+int ep_batch_knee(const int64_t* ms, const double* ms_per_pass, int count, double tol,
+                  int64_t* m_C, double* knee);
 
 /* Enable (1) / disable (0, default) host-side validation of batch indices
  * in ep_step (copies t to the host and synchronises). */

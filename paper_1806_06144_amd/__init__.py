@@ -95,6 +95,8 @@ def _load():
         "ep_batch_sweep": (I, [P, P, I, I, P]),
         "ep_resource_batch": (I, [P, ctypes.c_double, ctypes.POINTER(I64), ctypes.POINTER(I64),
                                   ctypes.POINTER(I64)]),
+        "ep_batch_knee": (I, [P, P, I, ctypes.c_double, ctypes.POINTER(I64),
+                              ctypes.POINTER(ctypes.c_double)]),
         "ep_timing_enable": (I, [P, I]),
         "ep_timing_read": (I, [P, ctypes.POINTER(EpTiming)]),
         "ep_sync": (I, [P]),
@@ -297,6 +299,19 @@ def ep_resource_batch(ctx, tol=0.1):
     mc, ms, mg = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     _check(_lib.ep_resource_batch(ctx, tol, ctypes.byref(mc), ctypes.byref(ms), ctypes.byref(mg)))
     return mc.value, ms.value, mg.value
+
+
+def ep_batch_knee(ms, ms_per_pass, tol=0.1):
+    """(m_C, knee) of a time-per-iteration curve (host only)."""
+    import numpy as np
+    m = np.ascontiguousarray(np.asarray(ms, dtype=np.int64))
+    t = np.ascontiguousarray(np.asarray(ms_per_pass, dtype=np.float64))
+    if m.shape != t.shape:
+        raise ValueError("ms and ms_per_pass differ in length")
+    mc, kn = ctypes.c_int64(), ctypes.c_double()
+    _check(_lib.ep_batch_knee(m.ctypes.data, t.ctypes.data, m.shape[0], tol, ctypes.byref(mc),
+                              ctypes.byref(kn)))
+    return mc.value, kn.value
 
 
 def ep_set_checks(ctx, on):

@@ -1067,33 +1067,91 @@ int ep_batch_sweep(ep_ctx* c, const int64_t* ms, int count, int reps, double* ms
     return rc;
 }
 
+int ep_batch_knee(const int64_t* ms, const double* t, int count, double tol, int64_t* m_C,
+                  double* knee) {
+    g_err.clear();
+    if (!ms || !t || count < 2) return fail(EP_EINVAL, "need two or more batch sizes");
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(EP_EINVAL, "tol must be in [0, 1)");
+    for (int i = 0; i < count; ++i) {
+        if (ms[i] < 1 || (i > 0 && ms[i] <= ms[i - 1]))
+            return fail(EP_EINVAL, "batch sizes must be positive and increasing");
+        if (!(t[i] > 0.0) || !std::isfinite(t[i]))
+            return fail(EP_EINVAL, "times must be positive and finite");
+    }
+    // Section 3 Step 1: time per iteration is flat up to the batch that
+    // fills the device, then linear. Fit log t = max(log t0, log a + log m):
+    // for each split j (points < j flat, >= j linear; j = 0: all linear,
+    // j = count: all flat) t0 and a are the geometric means of t and t/m
+    // over their parts; the split with the least squared log residual
+    // gives the knee t0 / a.
+    std::vector<double> lt(count), lm(count);
+    for (int i = 0; i < count; ++i) {
+        lt[i] = std::log(t[i]);
+        lm[i] = std::log((double)ms[i]);
+    }
+    double best = 1e300, best_knee = (double)ms[0];
+    for (int j = 0; j <= count; ++j) {
+        double s0 = 0.0, s1 = 0.0;
+        for (int i = 0; i < j; ++i) s0 += lt[i];
+        for (int i = j; i < count; ++i) s1 += lt[i] - lm[i];
+        const double l0 = j > 0 ? s0 / j : -1e300;
+        const double la = j < count ? s1 / (count - j) : -1e300;
+        double res = 0.0;
+        for (int i = 0; i < count; ++i) {
+            const double f = std::max(l0, la + lm[i]);
+            res += (lt[i] - f) * (lt[i] - f);
+        }
+        double k;
+        if (j == 0) k = (double)ms[0];
+        else if (j == count) k = (double)ms[count - 1];
+        else k = std::exp(l0 - la);
+        if (res < best - 1e-12) {
+            best = res;
+            best_knee = k;
+        }
+    }
+    const double target = (1.0 - tol) * best_knee;
+    int64_t mc = 1;
+    while ((double)mc < target && mc < (int64_t(1) << 40)) mc *= 2;
+    mc = std::max(ms[0], std::min(ms[count - 1], mc));
+    if (m_C) *m_C = mc;
+    if (knee) *knee = best_knee;
+    return EP_OK;
+}
+
 int ep_resource_batch(ep_ctx* c, double tol, int64_t* m_C, int64_t* m_S, int64_t* m_G) {
     g_err.clear();
     if (!c) return fail(EP_EINVAL, "ctx is NULL");
-    if (!(tol > 0.0 && tol < 1.0)) return fail(EP_EINVAL, "tol must be in (0, 1)");
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(EP_EINVAL, "tol must be in [0, 1)");
     DeviceGuard dg(c->device);
     // Section 3 Step 1. m_S: batch at which the paper's memory model
-    // (d + l + m) n floats fills the device; m_C: the smallest batch whose
-    // kernel-entry throughput is within tol of the best measured, i.e. where
-    // time per step stops being flat.
+    // (d + l + m) n floats fills the device; m_C: the knee of time per
+    // iteration against batch size, from the medians of three sweeps.
     hipDeviceProp_t prop;
     HIP_TRY(hipGetDeviceProperties(&prop, c->device));
     const double floats = (double)prop.totalGlobalMem / 4.0;
     const int64_t ms_cap = (int64_t)(floats / (double)c->n) - c->d - c->l;
     std::vector<int64_t> grid;
-    for (int64_t m = 32; m <= std::min<int64_t>(c->n, 32768); m *= 2) grid.push_back(m);
-    if (grid.empty()) grid.push_back(c->n);
-    std::vector<double> t(grid.size());
-    int rc = ep_batch_sweep(c, grid.data(), (int)grid.size(), 2, t.data());
-    if (rc) return rc;
-    double best = 0.0;
-    for (size_t i = 0; i < grid.size(); ++i) best = std::max(best, (double)grid[i] / t[i]);
-    int64_t mc = grid.back();
-    for (size_t i = 0; i < grid.size(); ++i)
-        if ((double)grid[i] / t[i] >= (1.0 - tol) * best) {
-            mc = grid[i];
-            break;
+    for (int64_t m = 16; m <= std::min<int64_t>(c->n, 32768); m *= 2) grid.push_back(m);
+    int64_t mc = c->n;
+    if (grid.size() >= 2) {
+        const int sweeps = 3;
+        std::vector<double> t(grid.size() * sweeps);
+        for (int r = 0; r < sweeps; ++r) {
+            int rc = ep_batch_sweep(c, grid.data(), (int)grid.size(), 3, t.data() + r * grid.size());
+            if (rc) return rc;
         }
+        std::vector<double> med(grid.size());
+        for (size_t i = 0; i < grid.size(); ++i) {
+            double v[3] = {t[i], t[i + grid.size()], t[i + 2 * grid.size()]};
+            std::sort(v, v + 3);
+            med[i] = v[1];
+        }
+        int rc = ep_batch_knee(grid.data(), med.data(), (int)grid.size(), tol, &mc, nullptr);
+        if (rc) return rc;
+    } else if (!grid.empty()) {
+        mc = grid[0];
+    }
     if (m_C) *m_C = mc;
     if (m_S) *m_S = std::max<int64_t>(1, ms_cap);
     if (m_G) *m_G = std::max<int64_t>(1, std::min(mc, ms_cap));
