@@ -551,6 +551,8 @@ def main():
     ap.add_argument("--blocked-compare", action="store_true",
                     help="also time the opt-in blocked form (kernel block written per centre "
                          "chunk) on the same batches, after the headline")
+    ap.add_argument("--no-blocked-compare", dest="blocked_compare", action="store_false",
+                    help="do not time the blocked form (the default)")
     ap.add_argument("--s", type=int, default=None,
                     help="override the subsample size (experiments only)")
     ap.add_argument("--shard", type=int, default=1,
