@@ -170,7 +170,8 @@ int run_kmv(ep_ctx* c, const float* Q, int64_t ldq, const float* qn, const int64
             int64_t nc, const float* W, int* slices, int64_t* rows_pad, bool timed,
             bool subsample, bool capture = false) {
     *rows_pad = round_up(std::max<int64_t>(nq, 1), kBM);
-    KmvPlan plan = kmv_plan(nq, nc, ldc, c->l_pad, c->kind, max_slices_for(*rows_pad, c->l_pad));
+    KmvPlan plan =
+        kmv_plan(nq, nc, ldc, c->l_pad, c->l, c->kind, max_slices_for(*rows_pad, c->l_pad));
     *slices = plan.slices();
     HIP_TRY(c->part.ensure((size_t)plan.slices() * (size_t)(*rows_pad) * c->l_pad * sizeof(float)));
     KmvArgs a{};
@@ -923,7 +924,7 @@ int ep_predict_noalloc(ep_ctx* c, const float* Z, int64_t n_z, float* out) {
             nq = std::min<int64_t>(n_z - z0, tq * kBM);
             rows_pad = round_up(nq, kBM);
             const int64_t max_sl = (cap - rows_pad) / (rows_pad * L);
-            plan = kmv_plan(nq, c->n, c->d, L, c->kind, (int)std::min<int64_t>(max_sl, 256));
+            plan = kmv_plan(nq, c->n, c->d, L, c->l, c->kind, (int)std::min<int64_t>(max_sl, 256));
             if (max_sl >= 1 && plan.slices() <= max_sl) break;
             if (tq == 1)
                 return fail(EP_EINVAL,

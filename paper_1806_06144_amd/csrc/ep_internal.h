@@ -67,11 +67,14 @@ struct KmvArgs {
 struct KmvPlan {
     int splits;
     int wl, wj;
-    int ltw;               // label tiles per wave (compile-time variant)
+    int ltw;               // 32-label tiles per wave (compile-time variant)
+    int lt16;              // > 0: 16-wide contraction on lt16 tiles of 16 labels
     int64_t cps;
     int slices() const { return splits * wj; }
 };
-KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices);
+// l: labels in use (weight columns >= l are zero, ldw >= l)
+KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int64_t l, int kind,
+                 int max_slices);
 // Whether a fused launch takes the vector body: d % 4 == 0 and every query
 // and centre row 16-byte aligned (the staged body serves the rest).
 inline bool kmv_vec(const float* Q, int64_t ldq, const float* C, int64_t ldc, int64_t d) {

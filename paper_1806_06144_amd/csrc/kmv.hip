@@ -50,6 +50,7 @@ namespace {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxLtw = 4;           // label tiles per wave (accumulator budget)
+constexpr int kMaxLt16 = 10;         // 16-label tiles of the 16-wide contraction
 
 // Register-staged body: 64 queries x 128 centres per iteration.
 constexpr int kSCSub = 4;
@@ -387,8 +388,13 @@ inline int batch_chunks(int64_t d) {
     return nchunk % 8 == 0 || nchunk % 8 > 4 ? 8 : 4;
 }
 
-template <int KIND, int LTW, int KRB>
+// LT16 = 0: contraction on 32-label tiles (32x32x2 MFMA), LTW tiles per
+// wave, waves in wl label groups x wj centre groups. LT16 > 0: contraction
+// on LT16 tiles of 16 labels (16x16x4 MFMA), waves in 2 query halves x 4
+// centre quarters (see below); LTW is unused.
+template <int KIND, int LTW, int KRB, int LT16>
 __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
+    constexpr bool k16 = LT16 > 0;
     constexpr int kRB = KRB;                 // chunks per batch
     constexpr int kRF = kRDC * kRB;          // features per batch
     constexpr int kQPR = kRF / 4;            // query quads per row and batch
@@ -396,7 +402,11 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     static_assert(kRB % kRP == 0, "the batch is staged in kRP-chunk parts");
     static_assert(kBM * kQPR == 2 * kThreads * (kRB / kRP), "two quads per thread and part");
     __shared__ __attribute__((aligned(16))) float qs[2][kBM * kRF];
+    // kernel values of the tile: for the 32-wide contraction in MFMA
+    // accumulator order, kb[centre sub-tile][query half][k row][lane]; for
+    // the 16-wide one kb16[centre][query ^ kswz(centre)]
     __shared__ float kb[kCSub][kQSub][16][64];
+    float (*kb16)[kBM] = reinterpret_cast<float (*)[kBM]>(&kb[0][0][0][0]);
     __shared__ float s_qn[kBM];
     __shared__ int64_t s_qid[kBM];
     __shared__ float s_cn[2][kBN];
@@ -457,15 +467,34 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
     const int gj = wave / p.wl;
     const int lb = gl * LTW * kTile;
     const int lvalid = p.lt * kTile;
-    const bool active = wave < p.wl * p.wj && lb < lvalid;
+    const bool active = k16 || (wave < p.wl * p.wj && lb < lvalid);
+    // 16-wide contraction: query half qh (queries 32 qh .. +31, two blocks
+    // of 16), centre quarter cq (centres 64 cq .. +63 of the tile)
+    const int qh = wave & 1, cq = wave >> 1;
 
-    floatx16 facc[LTW][kQSub];
+    constexpr int kAcc32 = k16 ? 1 : LTW;
+    constexpr int kAcc16 = k16 ? LT16 : 1;
+    floatx16 facc[kAcc32][kQSub];
+    floatx4 acc16[2][kAcc16];
+    if constexpr (!k16) {
 #pragma unroll
-    for (int i = 0; i < LTW; ++i)
+        for (int i = 0; i < LTW; ++i)
 #pragma unroll
-        for (int b = 0; b < kQSub; ++b)
+            for (int b = 0; b < kQSub; ++b)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
+                for (int v = 0; v < 16; ++v) facc[i][b][v] = 0.f;
+    } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int a = 0; a < LT16; ++a)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc16[h][a][i] = 0.f;
+    }
+    // position of query q of centre c in kb16: the XOR keeps both the
+    // epilogue's writes (centres 4 apart in one half-wave) and the
+    // contraction's reads (adjacent centres) on distinct banks
+    auto kswz = [](int c) { return 16 * (((c >> 2) ^ c) & 1); };
     // distances: 2 centre blocks x 4 query blocks of 16 x 16 (16x16x4 MFMA)
     floatx4 sacc[2][4];
 #pragma unroll
@@ -561,10 +590,30 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
 
     const int w_col = lb + LTW * (lane & 31);
     const int ldw4 = (int)p.ldw * 4;
-    const int w_voff = w_col < lvalid ? ((lane >> 5) << 2) * ldw4 + w_col * 4 : kOOB;
+    const int w_voff = k16 ? ((lane >> 4) * (int)p.ldw + LT16 * (lane & 15)) * 4
+                     : (w_col < lvalid ? ((lane >> 5) << 2) * ldw4 + w_col * 4 : kOOB);
     auto w_soff = [&](int jt, int v) { return (jt * 32 + ((v >> 2) << 3) + (v & 3)) * ldw4; };
-    constexpr int PD = LTW <= 2 ? 16 : 2;
-    float wbuf[PD][LTW];
+    constexpr int PD = k16 ? 2 : (LTW <= 2 ? 16 : 2);
+    constexpr int kWb = k16 ? LT16 : LTW;
+    float wbuf[PD][kWb];
+    // 16-wide contraction, k-step st (centres 64 cq + 4 st .. +3): lane l
+    // feeds k slot l/16 (that centre's row) and, for label tile a, row
+    // l%16 of the tile, i.e. label LT16 (l%16) + a: LT16 contiguous floats
+    // of one weight row (16 LT16 <= ldw, so they stay in the row)
+    auto load_w16 = [&](__amdgpu_buffer_rsrc_t r, int st, float* dst) {
+        const int so = (64 * cq + 4 * st) * ldw4;
+#pragma unroll
+        for (int a = 0; a + 4 <= kWb; a += 4) {
+            const float4 v = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(r, w_voff + 4 * a, so, 0));
+            dst[a] = v.x;
+            dst[a + 1] = v.y;
+            dst[a + 2] = v.z;
+            dst[a + 3] = v.w;
+        }
+#pragma unroll
+        for (int a = kWb & ~3; a < kWb; ++a) dst[a] = ld1(r, w_voff + 4 * a, so);
+    };
     // The weight rows of a k-step sit in soffset, which the range check does
     // not see; the descriptor spans the whole padded tile (kBN rows and the
     // 16-byte tail every weight matrix carries), which the caller's weights
@@ -584,7 +633,10 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         const __amdgpu_buffer_rsrc_t wrs = w_rsrc(tile);
         auto first_weights = [&]() {
 #pragma unroll
-            for (int v = 0; v < PD; ++v) load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+            for (int v = 0; v < PD; ++v) {
+                if constexpr (k16) load_w16(wrs, v, wbuf[v]);
+                else load_w<LTW>(wrs, w_voff, w_soff(gj, v), wbuf[v]);
+            }
         };
         if (LTW < 4 && active) first_weights();
         const float* cn = s_cn[tile & 1];
@@ -610,7 +662,12 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
                     float kv = kernel_value<KIND>(qnb + cn[cbase + 16 * cb + i] - 2.f * sacc[cb][qb][i],
                                                   p.scale);
                     if (dq == 16 * cb + i) kv = 1.f;
-                    kb[ct_s][qb >> 1][8 * cb + 4 * (q4 >> 1) + i][lk] = kv;
+                    if constexpr (k16) {
+                        const int cc = cbase + 16 * cb + i;
+                        kb16[cc][bl ^ kswz(cc)] = kv;
+                    } else {
+                        kb[ct_s][qb >> 1][8 * cb + 4 * (q4 >> 1) + i][lk] = kv;
+                    }
                 }
         }
         // Subsample centres (kpos >= 0): their kernel values also go to row
@@ -628,7 +685,10 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
                     const int r = __builtin_ctzll(flagged);
                     flagged &= flagged - 1;
                     const int pos = __builtin_amdgcn_readfirstlane(cp[r]);
-                    const float v = kcol[(4 * (r >> 3) + (r & 3)) * 64 + 32 * ((r >> 2) & 1)];
+                    const int cr = ct_s * 32 + r;
+                    const float v =
+                        k16 ? kb16[cr][lane ^ kswz(cr)]
+                            : kcol[(4 * (r >> 3) + (r & 3)) * 64 + 32 * ((r >> 2) & 1)];
                     // (the store takes its data as 32 raw bits)
                     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ks,
                                                           lane * 4, (int)((pos * p.ldk + q0) * 4), 0);
@@ -638,7 +698,39 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         if (tile + 1 < ntile) load_centre_meta(tile + 1);
         wg_barrier<-1>();
         if (p.cid && tile + 1 < ntile) find_diag(tile + 1);
-        if (active) {
+        if constexpr (k16) {
+            // out^T(labels x queries) += W^T K over this wave's 64 centres,
+            // four per 16x16x4 step, for its two query blocks; the kernel
+            // values are read two k-steps ahead
+            float kvr[2][2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int cc = 64 * cq + 4 * u + q4;
+                    kvr[u][h] = kb16[cc][(32 * qh + 16 * h + (lane & 15)) ^ kswz(cc)];
+                }
+#pragma unroll
+            for (int st = 0; st < 16; ++st) {
+                float wc[kWb];
+#pragma unroll
+                for (int a = 0; a < kWb; ++a) wc[a] = wbuf[st % PD][a];
+                if (st + PD < 16) load_w16(wrs, st + PD, wbuf[st % PD]);
+                const float kv0 = kvr[st & 1][0], kv1 = kvr[st & 1][1];
+                if (st + 2 < 16) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int cc = 64 * cq + 4 * (st + 2) + q4;
+                        kvr[st & 1][h] = kb16[cc][(32 * qh + 16 * h + (lane & 15)) ^ kswz(cc)];
+                    }
+                }
+#pragma unroll
+                for (int a = 0; a < kWb; ++a) {
+                    acc16[0][a] = __builtin_amdgcn_mfma_f32_16x16x4f32(wc[a], kv0, acc16[0][a], 0, 0, 0);
+                    acc16[1][a] = __builtin_amdgcn_mfma_f32_16x16x4f32(wc[a], kv1, acc16[1][a], 0, 0, 0);
+                }
+            }
+        } else if (active) {
             if (LTW == 4) first_weights();
             for (int jt = gj; jt < kCSub; jt += p.wj) {
 #pragma unroll
@@ -731,7 +823,20 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
         finish_tile(tile);
     }
 
-    if (active) {
+    if constexpr (k16) {
+        // element i of tile a, block h: label LT16 (4 (l/16) + i) + a,
+        // query 32 qh + 16 h + l%16; slice = (split, centre quarter)
+        const int slice = split * 4 + cq;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            float* o = p.out +
+                       ((int64_t)slice * p.out_rows + q0 + 32 * qh + 16 * h + (lane & 15)) * p.ldw;
+#pragma unroll
+            for (int a = 0; a < LT16; ++a)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[LT16 * (4 * q4 + i) + a] = acc16[h][a][i];
+        }
+    } else if (active) {
         const int slice = split * p.wj + gj;
         float* o = p.out + ((int64_t)slice * p.out_rows + q0) * p.ldw;
 #pragma unroll
@@ -751,14 +856,15 @@ __device__ __forceinline__ void kmv_body_vec(const KmvArgs& p) {
 // Two entry points with one body, so that profiles tell the predictions pass
 // (Algorithm 1 step 2, and prediction) from the subsample pass (steps 4-5).
 // KRB: chunks per batch of the vector body (unused by the staged one).
-template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2, int KRB>
+// LT16 > 0 (vector body, predictions pass only): the 16-wide contraction.
+template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2, int KRB, int LT16 = 0>
 __global__ void __launch_bounds__(kThreads) kmv_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB, LT16>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 template <int KIND, int LTW, bool VEC, int PF, int DC, bool ACC2, int KRB>
 __global__ void __launch_bounds__(kThreads) kmv_subsample_kernel(KmvArgs p) {
-    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB>(p);
+    if constexpr (VEC) kmv_body_vec<KIND, LTW, KRB, 0>(p);
     else kmv_body_staged<KIND, LTW, VEC, PF, DC, ACC2>(p);
 }
 
@@ -774,6 +880,28 @@ KmvFn pick(int ltw, bool sub) {
     }
 }
 
+template <int KIND, int KRB>
+KmvFn pick16(int lt16) {
+    switch (lt16) {
+        case 1: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 1>;
+        case 2: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 2>;
+        case 3: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 3>;
+        case 4: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 4>;
+        case 5: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 5>;
+        case 6: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 6>;
+        case 7: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 7>;
+        case 8: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 8>;
+        case 9: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 9>;
+        default: return kmv_kernel<KIND, 1, true, 1, 64, false, KRB, 10>;
+    }
+}
+
+// The 16-wide contraction's vector-body kernel for lt16 tiles of 16 labels
+KmvFn kernel16_for(int kind, int lt16, int krb) {
+    if (kind == 0) return krb == 8 ? pick16<0, 8>(lt16) : pick16<0, 4>(lt16);
+    return krb == 8 ? pick16<1, 8>(lt16) : pick16<1, 4>(lt16);
+}
+
 // krb: chunks per batch of the vector body (batch_chunks), 4 or 8
 KmvFn kernel_for(int kind, int ltw, bool vec, bool sub, int krb) {
     if (!vec) return kind == 0 ? pick<0, false, 4>(ltw, sub) : pick<1, false, 4>(ltw, sub);
@@ -781,7 +909,7 @@ KmvFn kernel_for(int kind, int ltw, bool vec, bool sub, int krb) {
     return krb == 8 ? pick<1, true, 8>(ltw, sub) : pick<1, true, 4>(ltw, sub);
 }
 
-int occupancy_slots(int kind, int ltw) {
+int occupancy_slots(KmvFn fn) {
     static int cus = -1;
     if (cus < 0) {
         int dev = 0;
@@ -792,8 +920,7 @@ int occupancy_slots(int kind, int ltw) {
             cus = prop.multiProcessorCount;
     }
     int per = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel_for(kind, ltw, true, false, 8),
-                                                     kThreads, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, kThreads, 0) != hipSuccess ||
         per < 1)
         per = 1;
     return per * cus;
@@ -808,7 +935,8 @@ float kernel_scale(int kind, float bandwidth) {
     return (float)(-log2e / bw);
 }
 
-KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int max_slices) {
+KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int64_t l, int kind,
+                 int max_slices) {
     KmvPlan best{};
     const int lt = (int)std::min<int64_t>(ldw / kTile, 32);
     const int64_t nct = ceil_div(std::max<int64_t>(nc, 1), kBN);
@@ -831,7 +959,21 @@ KmvPlan kmv_plan(int64_t nq, int64_t nc, int64_t ldc, int64_t ldw, int kind, int
             best.ltw = ltw;
         }
     }
-    const int slots = occupancy_slots(kind, best.ltw);
+    // Up to 160 labels (and with the vector body) the contraction runs on
+    // ceil(l / 16) tiles of 16 labels instead: no label padding beyond 15,
+    // waves as 2 query halves x 4 centre quarters. Layout and tiles per wave
+    // for the 32-wide bodies that serve the same launch otherwise (staged
+    // body, subsample pass) follow the same 2 x 4 split.
+    const int64_t lt16 = ceil_div(std::max<int64_t>(l, 1), 16);
+    best.lt16 = 0;
+    if (lt16 <= kMaxLt16 && 16 * lt16 <= ldw) {
+        best.lt16 = (int)lt16;
+        best.wl = 2;
+        best.wj = 4;
+        best.ltw = (int)ceil_div(lt, 2);
+    }
+    const int slots = occupancy_slots(best.lt16 ? kernel16_for(kind, best.lt16, 8)
+                                                : kernel_for(kind, best.ltw, true, false, 8));
     const int64_t tq = ceil_div(std::max<int64_t>(nq, 1), kBM);
     // splits of the centre axis: minimise the makespan of tq * splits equal
     // workgroups over the resident slots. A split's centre rows must stay
@@ -893,7 +1035,10 @@ hipError_t kmv_launch(KmvArgs a, const KmvPlan& p, hipStream_t s, bool subsample
         b.out = a.out + (int64_t)t0 * kTile;
         b.lt = std::min(32, lt_total - t0);
         if (t0 > 0) b.kpos = nullptr;
-        hipLaunchKernelGGL(kernel_for(a.kind, p.ltw, vec, subsample, batch_chunks(a.d)), grid,
+        const KmvFn fn = p.lt16 > 0 && vec && !subsample && lt_total <= 32
+                             ? kernel16_for(a.kind, p.lt16, batch_chunks(a.d))
+                             : kernel_for(a.kind, p.ltw, vec, subsample, batch_chunks(a.d));
+        hipLaunchKernelGGL(fn, grid,
                            dim3(kThreads), 0, s,
                            b);
         const hipError_t e = hipGetLastError();

@@ -22,6 +22,13 @@ CASES = [
     # wave, one of them partly empty)
     ("laplacian", 3000, 48, 70, 300, 30, 200, 2.0),
     ("gaussian", 2600, 96, 200, 256, 25, 300, 1.5),
+    # 16-wide contraction (l <= 160): tiles of 16 labels exactly full (16,
+    # 144 = 9 x 16) or one label past a tile (17), 7 and 10 tiles
+    ("gaussian", 1500, 40, 16, 200, 20, 150, 1.2),
+    ("laplacian", 1500, 40, 17, 200, 20, 150, 1.2),
+    ("laplacian", 1800, 36, 100, 256, 30, 200, 1.5),
+    ("gaussian", 2200, 44, 144, 300, 30, 260, 1.4),
+    ("gaussian", 1300, 52, 150, 200, 25, 129, 1.1),
     # batches of exactly one and two 512-row chunks for the product of
     # steps 4-5 (subsample of 192 = 3 x 64 rows for V^T G)
     ("laplacian", 1200, 32, 5, 192, 20, 512, 1.0),

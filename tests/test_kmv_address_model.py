@@ -58,7 +58,31 @@ def _check(what, voff, soff, nbytes, extent, lo, hi, row_len=None, ld=None):
             raise Violation(f"{what}: load past the end of a row")
 
 
-def model_vec(nq, nc, d, ldw, lt, ltw, wl, wj, cps, soffset_rows=False, t0=0):
+def model_w16(ldw, lt16, w_lo, w_alloc):
+    """Weight loads of the 16-wide contraction for one tile: wave w takes
+    centre quarter w >> 1; lane l reads lt16 contiguous floats of row
+    64 cq + 4 st + l/16, starting at column lt16 (l % 16), as 16-byte loads
+    and 4-byte ones for the rest; row offsets of the k-step in soffset."""
+    lane = np.arange(64)
+    ldw4 = ldw * 4
+    wext = KBN * ldw * 4 + TAIL
+    voff0 = ((lane >> 4) * ldw + lt16 * (lane & 15)) * 4
+    for wave in range(8):
+        cq = wave >> 1
+        for st in range(16):
+            soff = (64 * cq + 4 * st) * ldw4
+            a = 0
+            while a < lt16:
+                nbytes = 16 if a + 4 <= lt16 else 4
+                voff = voff0 + 4 * a
+                _check("weight16", voff, soff, nbytes, wext, w_lo, w_alloc)
+                col = (voff % ldw4) + nbytes
+                if col.max() > ldw4:
+                    raise Violation("weight16: load past the end of a weight row")
+                a += 4 if nbytes == 16 else 1
+
+
+def model_vec(nq, nc, d, ldw, lt, ltw, wl, wj, cps, soffset_rows=False, t0=0, lt16=0):
     """All loads of one vector-body launch (every query tile and split)."""
     ldq = ldc = d
     krb = batch_chunks(d)
@@ -120,6 +144,10 @@ def model_vec(nq, nc, d, ldw, lt, ltw, wl, wj, cps, soffset_rows=False, t0=0):
                             voff = np.where(ok, c_voff + cbk * c_blk, KOOB)
                             soff = f0 * 4
                         _check("centre", voff, soff, 16, ext, c0 * ldc * 4, c_alloc, d, ldc)
+                if lt16:
+                    if wave == 0:
+                        model_w16(ldw, lt16, c0 * ldw * 4, w_alloc)
+                    continue
                 # weights of this wave's contraction role
                 gl, gj = wave % wl, wave // wl
                 lb = gl * ltw * KTILE
@@ -164,6 +192,11 @@ def test_vector_body_loads_stay_inside_the_callers_buffers(nq, nc, d, l):
         for P in sorted({1, min(2, nct), nct}):
             cps = -(-nct // P) * KBN
             model_vec(nq, nc, d, ldw, lt, ltw, wl, wj, cps)
+    lt16 = -(-l // 16)
+    if lt16 <= 10:
+        for P in sorted({1, nct}):
+            cps = -(-nct // P) * KBN
+            model_vec(nq, nc, d, ldw, lt, -(-lt // 2), 2, 4, cps, lt16=lt16)
 
 
 def test_model_sees_rows_in_soffset():
@@ -185,3 +218,17 @@ def test_label_blocks_beyond_1024_stay_inside():
     lt = lt_total - t0
     for ltw, wl, wj in layouts(lt):
         model_vec(70, 300, 8, ldw, lt, ltw, wl, wj, 512, t0=t0)
+
+
+@pytest.mark.parametrize("l", [1, 5, 10, 16, 17, 33, 48, 70, 100, 129, 144, 150, 160])
+def test_weight_loads_of_the_16_wide_contraction(l):
+    """Every weight load of the 16-wide contraction (l <= 160) lies in the
+    padded tile of weight rows and inside one row."""
+    ldw = -(-l // KTILE) * KTILE
+    lt16 = -(-l // 16)
+    assert 16 * lt16 <= ldw
+    nc = 700
+    w_rows = -(-nc // KBN) * KBN
+    w_alloc = w_rows * ldw * 4 + TAIL
+    for c0 in range(0, nc, KBN):
+        model_w16(ldw, lt16, c0 * ldw * 4, w_alloc)
