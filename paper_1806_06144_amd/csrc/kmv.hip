@@ -30,6 +30,9 @@
 //      runs on the same MFMA with W read straight from global memory (a few
 //      k-steps ahead). The label tiles are spread over the 8 waves so that
 //      the accumulators of up to 1024 labels fit in 128 registers per lane.
+//      Up to 160 labels the vector body contracts on tiles of 16 labels
+//      instead (v_mfma_f32_16x16x4f32, no label padding beyond 15), with
+//      the kernel values in LDS as [centre][query].
 //   4. Optionally (kpos, step 2 of the vector body) the kernel values of the
 //      centres that are subsample points are also stored, column by column,
 //      so that steps 4-5 need no second pass over those m x s entries (the
