@@ -29,6 +29,8 @@ CASES = [
     ("laplacian", 1800, 36, 100, 256, 30, 200, 1.5),
     ("gaussian", 2200, 44, 144, 300, 30, 260, 1.4),
     ("gaussian", 1300, 52, 150, 200, 25, 129, 1.1),
+    # first label count past the 16-wide contraction (161: 32-wide again)
+    ("laplacian", 1400, 36, 161, 200, 20, 150, 1.3),
     # batches of exactly one and two 512-row chunks for the product of
     # steps 4-5 (subsample of 192 = 3 x 64 rows for V^T G)
     ("laplacian", 1200, 32, 5, 192, 20, 512, 1.0),

@@ -31,6 +31,7 @@ def _both(g, Z):
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("kernel,n,d,l", [("gaussian", 5000, 64, 10),
+                                          ("gaussian", 4100, 48, 144),
                                           ("laplacian", 3001, 37, 1100)])
 def test_noalloc_predict_matches_predict(kernel, n, d, l):
     X, a, rng = _problem(n, d, l, 3)
