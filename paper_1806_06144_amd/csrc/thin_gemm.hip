@@ -15,7 +15,9 @@
 // transpose of a row-major (depth x M) matrix. A workgroup of 4 waves owns
 // a 64 x 64 output tile, each wave a 32 x 32 block on
 // v_mfma_f32_32x32x2f32; operands are staged through LDS in 32-deep stages
-// (depth-major, so a lane's operand read is one conflict-free LDS word).
+// (depth-major, so a lane's operand read is one conflict-free LDS word),
+// two stages deep: the next stage is fetched while the current one feeds
+// the MFMAs.
 // Depth is split into chunks (`kc`, one partial slice each, summed by the
 // reduction kernels in slice order) so that enough workgroups exist, and
 // inside a chunk the accumulation is blocked: the MFMA accumulator is
@@ -55,8 +57,10 @@ __device__ __forceinline__ float4 ld4(const float* row, int64_t j0, int64_t len)
 
 template <bool A_T, bool SCATTER>
 __global__ void __launch_bounds__(kGThreads) thin_gemm_kernel(ThinGemmArgs p) {
-    __shared__ float As[kKS][kTM + kPadA];
-    __shared__ float Bs[kKS][kTN + kPadB];
+    // two LDS stages: the next stage's operands are fetched into registers
+    // while the MFMAs read the current one, so one barrier per stage
+    __shared__ float As[2][kKS][kTM + kPadA];
+    __shared__ float Bs[2][kKS][kTN + kPadB];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -76,52 +80,63 @@ __global__ void __launch_bounds__(kGThreads) thin_gemm_kernel(ThinGemmArgs p) {
         acc[v] = 0.f;
         sum[v] = 0.f;
     }
-    int in_block = 0;
-    for (int64_t k0 = k_lo; k0 < k_hi; k0 += kKS) {
-        const int64_t kd = min((int64_t)kKS, k_hi - k0);   // valid depth of this stage
-        // A tile: 64 rows x 32 depth -> As[depth][row]
-        if (A_T) {
-            // A(i, kk) = A[kk * lda + i]: rows of the stored matrix run along i
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const int q = tid + e * kGThreads;        // 512 quads of (depth, 4 rows)
-                const int kk = q / (kTM / 4), ii = 4 * (q % (kTM / 4));
-                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (kk < kd) v = ld4(p.A + (k0 + kk) * p.lda + i0, ii, p.M - i0);
-                *reinterpret_cast<float4*>(&As[kk][ii]) = v;
-            }
-        } else {
-            // A(i, kk) = A[i * lda + kk]: rows of the stored matrix run along kk
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const int q = tid + e * kGThreads;        // 512 quads of (row, 4 depth)
-                const int ii = q / (kKS / 4), kk = 4 * (q % (kKS / 4));
-                float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (i0 + ii < p.M) v = ld4(p.A + (i0 + ii) * p.lda + k0, kk, kd);
-                As[kk][ii] = v.x;
-                As[kk + 1][ii] = v.y;
-                As[kk + 2][ii] = v.z;
-                As[kk + 3][ii] = v.w;
-            }
-        }
-        // B tile: 32 depth x 64 columns -> Bs[depth][col]
+    // this thread's share of a stage: two quads of A, two of B
+    float4 ra[2], rb[2];
+    auto fetch = [&](int64_t k0) {
+        const int64_t kd = min((int64_t)kKS, k_hi - k0);   // valid depth of the stage
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             const int q = tid + e * kGThreads;
+            ra[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (A_T) {
+                // A(i, kk) = A[kk * lda + i]: quad of (depth, 4 rows)
+                const int kk = q / (kTM / 4), ii = 4 * (q % (kTM / 4));
+                if (kk < kd) ra[e] = ld4(p.A + (k0 + kk) * p.lda + i0, ii, p.M - i0);
+            } else {
+                // A(i, kk) = A[i * lda + kk]: quad of (row, 4 depth)
+                const int ii = q / (kKS / 4), kk = 4 * (q % (kKS / 4));
+                if (i0 + ii < p.M) ra[e] = ld4(p.A + (i0 + ii) * p.lda + k0, kk, kd);
+            }
             const int kk = q / (kTN / 4), jj = 4 * (q % (kTN / 4));
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (kk < kd) v = ld4(p.B + (k0 + kk) * p.ldb + j0, jj, p.N - j0);
-            *reinterpret_cast<float4*>(&Bs[kk][jj]) = v;
+            rb[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (kk < kd) rb[e] = ld4(p.B + (k0 + kk) * p.ldb + j0, jj, p.N - j0);
         }
+    };
+    // A tile -> As[depth][row], B tile -> Bs[depth][col]
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int q = tid + e * kGThreads;
+            if (A_T) {
+                const int kk = q / (kTM / 4), ii = 4 * (q % (kTM / 4));
+                *reinterpret_cast<float4*>(&As[buf][kk][ii]) = ra[e];
+            } else {
+                const int ii = q / (kKS / 4), kk = 4 * (q % (kKS / 4));
+                As[buf][kk][ii] = ra[e].x;
+                As[buf][kk + 1][ii] = ra[e].y;
+                As[buf][kk + 2][ii] = ra[e].z;
+                As[buf][kk + 3][ii] = ra[e].w;
+            }
+            const int kk = q / (kTN / 4), jj = 4 * (q % (kTN / 4));
+            *reinterpret_cast<float4*>(&Bs[buf][kk][jj]) = rb[e];
+        }
+    };
+    int in_block = 0;
+    int buf = 0;
+    if (k_lo < k_hi) fetch(k_lo);
+    for (int64_t k0 = k_lo; k0 < k_hi; k0 += kKS, buf ^= 1) {
+        // the stage written here was last read two stages ago, before the
+        // previous barrier
+        stash(buf);
         __syncthreads();
+        if (k0 + kKS < k_hi) fetch(k0 + kKS);
         const int h = lane >> 5, r = lane & 31;
 #pragma unroll
         for (int s2 = 0; s2 < kKS / 2; ++s2) {
-            const float a = As[2 * s2 + h][wm * 32 + r];
-            const float b = Bs[2 * s2 + h][wn * 32 + r];
+            const float a = As[buf][2 * s2 + h][wm * 32 + r];
+            const float b = Bs[buf][2 * s2 + h][wn * 32 + r];
             acc = mfma(a, b, acc);
         }
-        __syncthreads();
         in_block += kKS;
         if (in_block == kBlk || k0 + kKS >= k_hi) {
 #pragma unroll
